@@ -1,0 +1,222 @@
+/*
+ * oracle_attn.c -- plain fp64 CPU oracle for scaled dot-product attention.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the bench's
+ * CPU-baseline leg may load this library.  It shares no code, header, helper or
+ * constant with the GPU library; the two meet only through the seeded inputs.
+ *
+ * What it computes (per batch b and head h independently, as the paper's
+ * remark on higher-rank tensors partitions the problem, Sec. "MoA DNF
+ * Derivation of Attention"):
+ *
+ *   Attention(Q, K, V) = softmax(scale * Q K^T) V          (eq. attention)
+ *
+ * with the numerically stable softmax of eq. stable_softmax.  For each query
+ * row i the steps are taken in the paper's order (Steps I-IV and eq.
+ * output_dnf; the per-row arrays s, e, w of Algorithm 1 are kept explicitly,
+ * every intermediate is materialised, nothing is fused or reordered):
+ *
+ *   s[k] = scale * sum_{j=0}^{dk-1} Q[i][j] * K[k][j]     (eq. mm_psi: K read by
+ *                                                            row, no K^T)
+ *          or -inf when key k is masked
+ *   m    = max_k s[k]                                      (Step I, eq. z_psi)
+ *   e[k] = exp(s[k] - m)          (0 for masked keys)      (Step II, eq. num_psi)
+ *   Z    = sum_k e[k]                                      (Step III, eq. den_psi)
+ *   w[k] = e[k] / Z                                        (Step IV)
+ *   O[i][c] = sum_k w[k] * V[k][c]                         (eq. output_dnf)
+ *
+ * Readings where the paper is silent (each also listed in the design notes):
+ *  - The paper divides by sqrt(dk); this oracle multiplies by a caller-given
+ *    fp32 `scale` (1/sqrt(dk) by default in the callers), widened exactly.
+ *  - Causal masking is not in the paper.  Key k is visible to query i iff
+ *    k <= i + (Nk - Nq) (bottom-right aligned; equal to k <= i when Nq == Nk).
+ *  - Masked logits are -inf, their e and w are exactly 0, and the max runs
+ *    over visible keys only.
+ *  - Sums run in increasing index order in IEEE fp64 with no contraction
+ *    (built with -ffp-contract=off, no fast-math).
+ *  - Inputs are fp32 or bf16 bit patterns; both widen exactly to fp64.
+ *
+ * Also returned on request: LSE[i] = m + ln(Z), the log of the softmax
+ * denominator in natural-log units, and the full S and P matrices for tiny
+ * shapes.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
+
+typedef struct {
+    const void* q;
+    const void* k;
+    const void* v;
+    int dtype;
+    int64_t B, H, Nq, Nk, dk, dv;
+    double scale;
+    int causal;
+} problem_t;
+
+/* Exact widening of one stored element to fp64. */
+static double elem(const void* base, int dtype, int64_t idx) {
+    if (dtype == ORACLE_F32) return (double)((const float*)base)[idx];
+    uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+static int visible(const problem_t* p, int64_t i, int64_t k) {
+    return !p->causal || k <= i + (p->Nk - p->Nq);
+}
+
+/*
+ * One query row: flat row index r = (b*H + h)*Nq + i.
+ * s, e, w are caller-provided scratch of length Nk (Algorithm 1's vectors).
+ * Writes O row (dv values), and optionally LSE, S row and P row.
+ */
+static void attend_row(const problem_t* p, int64_t r, double* s, double* e, double* w,
+                       double* o_row, double* lse, double* s_row, double* p_row) {
+    const int64_t bh = r / p->Nq;
+    const int64_t i = r % p->Nq;
+    const int64_t q_base = (bh * p->Nq + i) * p->dk;
+    const int64_t k_base = bh * p->Nk * p->dk;
+    const int64_t v_base = bh * p->Nk * p->dv;
+
+    /* scores: inner product of Q row i with K row k (eq. mm_psi), then scaled */
+    for (int64_t k = 0; k < p->Nk; ++k) {
+        if (!visible(p, i, k)) {
+            s[k] = -INFINITY;
+            continue;
+        }
+        double acc = 0.0;
+        for (int64_t j = 0; j < p->dk; ++j)
+            acc += elem(p->q, p->dtype, q_base + j) * elem(p->k, p->dtype, k_base + k * p->dk + j);
+        s[k] = p->scale * acc;
+    }
+    /* Step I: row maximum over visible keys */
+    double m = -INFINITY;
+    for (int64_t k = 0; k < p->Nk; ++k)
+        if (s[k] > m) m = s[k];
+    /* Step II: numerator */
+    for (int64_t k = 0; k < p->Nk; ++k)
+        e[k] = (s[k] == -INFINITY) ? 0.0 : exp(s[k] - m);
+    /* Step III: denominator */
+    double Z = 0.0;
+    for (int64_t k = 0; k < p->Nk; ++k) Z += e[k];
+    /* Step IV: attention weights */
+    for (int64_t k = 0; k < p->Nk; ++k) w[k] = e[k] / Z;
+    /* output row: weighted sum of V rows, each O[i][c] summed in increasing k */
+    for (int64_t c = 0; c < p->dv; ++c) o_row[c] = 0.0;
+    for (int64_t k = 0; k < p->Nk; ++k) {
+        if (s[k] == -INFINITY) continue;   /* masked key: its weight is exactly 0 */
+        for (int64_t c = 0; c < p->dv; ++c)
+            o_row[c] += w[k] * elem(p->v, p->dtype, v_base + k * p->dv + c);
+    }
+    if (lse) *lse = m + log(Z);
+    if (s_row) memcpy(s_row, s, (size_t)p->Nk * sizeof(double));
+    if (p_row) memcpy(p_row, w, (size_t)p->Nk * sizeof(double));
+}
+
+static int check(const problem_t* p) {
+    if (!p->q || !p->k || !p->v) return 1;
+    if (p->dtype != ORACLE_F32 && p->dtype != ORACLE_BF16) return 1;
+    if (p->B < 0 || p->H < 0 || p->Nq < 0 || p->Nk <= 0 || p->dk <= 0 || p->dv <= 0) return 1;
+    if (p->causal && p->Nq > p->Nk) return 1;
+    return 0;
+}
+
+static void set_threads(int nthreads) {
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+}
+
+/* Runs rows[0..n_rows) (flat row indices) or, if rows == NULL, all B*H*Nq rows. */
+static int run_rows(const problem_t* p, const int64_t* rows, int64_t n_rows, double* O, double* LSE,
+                    double* S, double* P, int nthreads) {
+    if (check(p)) return 1;
+    const int64_t total = p->B * p->H * p->Nq;
+    if (rows)
+        for (int64_t t = 0; t < n_rows; ++t)
+            if (rows[t] < 0 || rows[t] >= total) return 1;
+    set_threads(nthreads);
+    int nt = 1;
+#ifdef _OPENMP
+    nt = omp_get_max_threads();
+#endif
+    /* per-thread copies of Algorithm 1's row vectors s, e, w */
+    double* scratch = (double*)malloc((size_t)nt * 3 * (size_t)p->Nk * sizeof(double));
+    if (!scratch) return 2;
+#pragma omp parallel num_threads(nt)
+    {
+        int tid = 0;
+#ifdef _OPENMP
+        tid = omp_get_thread_num();
+#endif
+        double* s = scratch + (size_t)tid * 3 * (size_t)p->Nk;
+        double* e = s + p->Nk;
+        double* w = e + p->Nk;
+#pragma omp for schedule(dynamic, 4)
+        for (int64_t t = 0; t < n_rows; ++t) {
+            int64_t r = rows ? rows[t] : t;
+            attend_row(p, r, s, e, w, O + t * p->dv, LSE ? LSE + t : NULL,
+                       S ? S + t * p->Nk : NULL, P ? P + t * p->Nk : NULL);
+        }
+    }
+    free(scratch);
+    return 0;
+}
+
+/*
+ * Full problem.  Q [B][H][Nq][dk], K [B][H][Nk][dk], V [B][H][Nk][dv] (row-major,
+ * fp32 or bf16 bits per `dtype`).  O [B][H][Nq][dv] fp64; LSE [B][H][Nq] fp64 or NULL.
+ * Returns 0 on success, 1 on bad arguments, 2 on host allocation failure.
+ */
+int oracle_attn_fwd(const void* Q, const void* K, const void* V, int dtype, int64_t B, int64_t H,
+                    int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale, int causal,
+                    double* O, double* LSE, int nthreads) {
+    problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
+    if (!O) return 1;
+    return run_rows(&p, NULL, B * H * Nq, O, LSE, NULL, NULL, nthreads);
+}
+
+/*
+ * Selected rows only: rows[t] is the flat row (b*H + h)*Nq + i.  O_rows is
+ * [n_rows][dv], LSE_rows [n_rows] or NULL.  Used to check sampled outputs of
+ * the large workloads.
+ */
+int oracle_attn_rows(const void* Q, const void* K, const void* V, int dtype, int64_t B, int64_t H,
+                     int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale, int causal,
+                     const int64_t* rows, int64_t n_rows, double* O_rows, double* LSE_rows,
+                     int nthreads) {
+    problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
+    if (!O_rows || !rows || n_rows < 0) return 1;
+    return run_rows(&p, rows, n_rows, O_rows, LSE_rows, NULL, NULL, nthreads);
+}
+
+/*
+ * Full problem with the score matrix S (scaled, -inf where masked) and the
+ * attention weights P, both [B][H][Nq][Nk] fp64, for tiny shapes.
+ */
+int oracle_attn_weights(const void* Q, const void* K, const void* V, int dtype, int64_t B,
+                        int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale,
+                        int causal, double* S, double* P, double* O, double* LSE) {
+    problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
+    if (!S || !P || !O) return 1;
+    return run_rows(&p, NULL, B * H * Nq, O, LSE, S, P, 1);
+}
+
+/* Threads OpenMP would use for a call with nthreads <= 0. */
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

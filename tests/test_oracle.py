@@ -1,0 +1,257 @@
+"""Pins for the fp64 oracle (CPU only).
+
+Each test checks the oracle against something other than itself: the paper's
+printed worked example, a library routine (torch's fp64 scaled dot-product
+attention on the CPU), closed forms, or invariants of the definition.  Between
+them a dropped scale, a wrong sign, a transposed operand, a missing max
+subtraction, a wrong mask orientation or alignment, or a wrong bf16 widening
+fails at least one test.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+import synth
+
+torch.set_num_threads(2)
+
+
+def _load(golden_dir, name):
+    with open(os.path.join(golden_dir, name)) as f:
+        return json.load(f)
+
+
+def _as4(a):
+    return np.asarray(a, dtype=np.float32)[None, None]
+
+
+def _worked_example(golden_dir):
+    g = _load(golden_dir, "worked_example_n3_d4.json")
+    return g, _as4(g["Q"]), _as4(g["K"]), _as4(g["V"])
+
+
+# ---------------------------------------------------------------- paper pins
+
+def test_worked_example_tables(golden_dir):
+    g, q, k, v = _worked_example(golden_dir)
+    s, p, o, lse = oracle.attention_weights(q, k, v, scale=g["scale"])
+    # Table 1: attention weights; Table 2: output (both printed to 4 d.p.)
+    assert np.max(np.abs(p[0, 0] - np.array(g["P_table1"]))) < 2e-4
+    assert np.max(np.abs(o[0, 0] - np.array(g["O_table2"]))) < 2e-4
+    # Table 1's row sums are 1 (1.0001 is display rounding per its footnote)
+    assert np.max(np.abs(p[0, 0].sum(-1) - 1.0)) < 1e-14
+    assert np.max(np.abs(p[0, 0].sum(-1) - np.array(g["P_row_sums_table1"]))) <= 1.5e-4
+    # the full-problem entry point gives the same O
+    o2 = oracle.attention(q, k, v, scale=g["scale"])
+    assert np.array_equal(o, o2)
+
+
+def test_worked_example_row0_trace(golden_dir):
+    g, q, k, v = _worked_example(golden_dir)
+    t = _load(golden_dir, "worked_example_row0_trace.json")
+    s, p, o, lse = oracle.attention_weights(q, k, v, scale=g["scale"])
+    x = s[0, 0, 0]
+    m = x.max()
+    Z = np.exp(lse[0, 0, 0] - m)          # denominator recovered from the oracle's LSE
+    exp_z = p[0, 0, 0] * Z                # numerator recovered from the oracle's weights
+    assert np.max(np.abs(x / g["scale"] - np.array(t["s_unscaled"]))) < 3e-4
+    assert np.max(np.abs(x - np.array(t["x_scaled"]))) < 2e-4
+    assert abs(m - t["m"]) < 2e-4
+    assert np.max(np.abs((x - m) - np.array(t["z"]))) < 2e-4
+    assert np.max(np.abs(exp_z - np.array(t["exp_z"]))) < 2e-4
+    assert abs(Z - t["Z"]) < 2e-4
+    assert np.max(np.abs(p[0, 0, 0] - np.array(t["w"]))) < 2e-4
+    assert np.max(np.abs(o[0, 0, 0] - np.array(t["output_row0"]))) < 2e-4
+
+
+# ------------------------------------------------------------ library routine
+
+def _torch_sdpa(q, k, v, scale, causal):
+    def t(a):
+        if a.dtype == np.uint16:
+            return synth.to_torch(a).to(torch.float64)
+        return torch.from_numpy(a).to(torch.float64)
+    tq, tk, tv = t(q), t(k), t(v)
+    Nq, Nk = q.shape[2], k.shape[2]
+    mask = None
+    if causal:
+        # key k visible to query i iff k <= i + (Nk - Nq)
+        i = torch.arange(Nq)[:, None]
+        j = torch.arange(Nk)[None, :]
+        mask = j <= i + (Nk - Nq)
+    return F.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, scale=scale).numpy()
+
+
+SHAPES = [
+    # B, H, Nq, Nk, dk, dv
+    (1, 1, 1, 1, 4, 4),
+    (1, 2, 3, 5, 4, 6),
+    (2, 3, 17, 17, 64, 64),
+    (1, 2, 5, 31, 8, 3),
+    (2, 1, 33, 64, 64, 128),
+    (1, 1, 64, 64, 128, 128),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_matches_torch_sdpa_fp64(shape, causal, dtype):
+    B, H, Nq, Nk, dk, dv = shape
+    if causal and Nq > Nk:
+        pytest.skip("causal needs Nq <= Nk")
+    seed = 31 * sum(shape) + (7 if causal else 0) + (1 if dtype == "bf16" else 0)
+    q = synth.normal(seed, (B, H, Nq, dk), 1.0, dtype)
+    k = synth.normal(seed + 1, (B, H, Nk, dk), 1.0, dtype)
+    v = synth.normal(seed + 2, (B, H, Nk, dv), 1.0, dtype)
+    scale = float(np.float32(1.0 / np.sqrt(dk)))
+    o = oracle.attention(q, k, v, scale=scale, causal=causal)
+    ref = _torch_sdpa(q, k, v, scale, causal)
+    assert np.max(np.abs(o - ref)) < 1e-12
+
+
+def test_torch_causal_convention_when_square():
+    # With Nq == Nk the oracle's mask equals torch's own is_causal (key j <= query i).
+    q = synth.normal(1, (1, 2, 9, 16), 1.0, "f32")
+    k = synth.normal(2, (1, 2, 9, 16), 1.0, "f32")
+    v = synth.normal(3, (1, 2, 9, 16), 1.0, "f32")
+    ref = F.scaled_dot_product_attention(*(torch.from_numpy(a).double() for a in (q, k, v)),
+                                         is_causal=True, scale=0.25).numpy()
+    assert np.max(np.abs(oracle.attention(q, k, v, scale=0.25, causal=True) - ref)) < 1e-12
+
+
+def test_weights_and_lse_match_library():
+    q = synth.normal(40, (1, 2, 7, 16), 1.0, "f32")
+    k = synth.normal(41, (1, 2, 11, 16), 1.0, "f32")
+    v = synth.normal(42, (1, 2, 11, 5), 1.0, "f32")
+    s, p, o, lse = oracle.attention_weights(q, k, v, scale=0.25)
+    tq, tk = torch.from_numpy(q).double(), torch.from_numpy(k).double()
+    scores = (tq @ tk.transpose(-1, -2)) * 0.25
+    assert np.max(np.abs(s - scores.numpy())) < 1e-13
+    assert np.max(np.abs(p - torch.softmax(scores, -1).numpy())) < 1e-14
+    assert np.max(np.abs(lse - torch.logsumexp(scores, -1).numpy())) < 1e-13
+
+
+def test_large_logits_stay_finite():
+    # Logits of order 1e3: exp without the row-max subtraction of Step I overflows.
+    q = synth.normal(50, (1, 1, 32, 64), 30.0, "f32")
+    k = synth.normal(51, (1, 1, 48, 64), 30.0, "f32")
+    v = synth.normal(52, (1, 1, 48, 64), 1.0, "f32")
+    o, lse = oracle.attention(q, k, v, scale=0.125, with_lse=True)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    ref = _torch_sdpa(q, k, v, 0.125, False)
+    assert np.max(np.abs(o - ref)) < 1e-10
+
+
+# ------------------------------------------------------ closed forms, invariants
+
+@pytest.mark.parametrize("Nq,Nk,causal", [(16, 16, False), (16, 16, True), (5, 12, True), (9, 4, False)])
+def test_zero_query_gives_mean_of_visible_values(Nq, Nk, causal):
+    q = np.zeros((1, 2, Nq, 64), dtype=np.float32)
+    k = synth.normal(60, (1, 2, Nk, 64), 1.0, "f32")
+    v = synth.normal(61, (1, 2, Nk, 32), 1.0, "f32").astype(np.float64).astype(np.float32)
+    o = oracle.attention(q, k, v, causal=causal)
+    vd = v.astype(np.float64)
+    for i in range(Nq):
+        last = min(Nk, i + (Nk - Nq) + 1) if causal else Nk
+        want = vd[:, :, :last, :].mean(axis=2)
+        assert np.max(np.abs(o[:, :, i, :] - want)) < 1e-13
+
+
+def test_zero_scale_gives_column_mean():
+    q = synth.normal(62, (1, 1, 8, 64), 1.0, "f32")
+    k = synth.normal(63, (1, 1, 10, 64), 1.0, "f32")
+    v = synth.normal(64, (1, 1, 10, 64), 1.0, "f32")
+    o = oracle.attention(q, k, v, scale=0.0)
+    assert np.max(np.abs(o[0, 0] - v[0, 0].astype(np.float64).mean(0))) < 1e-13
+
+
+def test_single_key_and_causal_first_row():
+    q = synth.normal(70, (2, 2, 6, 64), 1.0, "bf16")
+    k = synth.normal(71, (2, 2, 1, 64), 1.0, "bf16")
+    v = synth.normal(72, (2, 2, 1, 64), 1.0, "bf16")
+    o = oracle.attention(q, k, v)
+    assert np.array_equal(o, np.broadcast_to(synth.bf16_bits_to_f32(v).astype(np.float64), o.shape))
+    k2 = synth.normal(73, (2, 2, 6, 64), 1.0, "bf16")
+    v2 = synth.normal(74, (2, 2, 6, 64), 1.0, "bf16")
+    o2 = oracle.attention(q, k2, v2, causal=True)
+    assert np.array_equal(o2[:, :, 0, :], synth.bf16_bits_to_f32(v2)[:, :, 0, :].astype(np.float64))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_one_hot_dominant_key(d):
+    Nq, Nk, kstar = 12, 40, 17
+    q = np.zeros((1, 1, Nq, d), dtype=np.float32)
+    q[..., 0] = 32.0
+    k = synth.normal(80, (1, 1, Nk, d), 1.0, "f32")
+    k[..., 0] = 0.0
+    k[0, 0, kstar, 0] = 32.0
+    v = synth.normal(81, (1, 1, Nk, d), 1.0, "f32")
+    o = oracle.attention(q, k, v)
+    want = np.broadcast_to(v[0, 0, kstar].astype(np.float64), (Nq, d))
+    assert np.max(np.abs(o[0, 0] - want)) < 1e-12
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_row_shift_invariance(causal):
+    # Augmented last dimension: K[..., -1] = 1, so Q[i, -1] = c adds scale*c to
+    # every logit of row i; the softmax must not change.
+    B, H, N, d = 1, 2, 24, 64
+    q = synth.normal(90, (B, H, N, d), 1.0, "f32")
+    k = synth.normal(91, (B, H, N, d), 1.0, "f32")
+    v = synth.normal(92, (B, H, N, d), 1.0, "f32")
+    k[..., -1] = 1.0
+    q[..., -1] = 0.0
+    oa = oracle.attention(q, k, v, causal=causal)
+    qb = q.copy()
+    qb[..., -1] = (2.0 ** (np.arange(N) % 11)).astype(np.float32)[None, None, :]
+    ob = oracle.attention(qb, k, v, causal=causal)
+    assert np.max(np.abs(oa - ob)) < 1e-12
+
+
+def test_joint_key_value_permutation_invariance():
+    q = synth.normal(100, (1, 2, 20, 64), 1.0, "f32")
+    k = synth.normal(101, (1, 2, 33, 64), 1.0, "f32")
+    v = synth.normal(102, (1, 2, 33, 64), 1.0, "f32")
+    perm = np.random.default_rng(0).permutation(33)
+    o = oracle.attention(q, k, v)
+    op = oracle.attention(q, k[:, :, perm], v[:, :, perm])
+    assert np.max(np.abs(o - op)) < 1e-13
+
+
+def test_constant_values_give_constant_output():
+    q = synth.normal(110, (1, 1, 16, 64), 2.0, "f32")
+    k = synth.normal(111, (1, 1, 16, 64), 2.0, "f32")
+    v = np.full((1, 1, 16, 64), 0.75, dtype=np.float32)
+    for causal in (False, True):
+        o = oracle.attention(q, k, v, causal=causal)
+        assert np.max(np.abs(o - 0.75)) < 1e-14
+
+
+def test_rows_entry_point_and_threads_agree():
+    q = synth.normal(120, (2, 3, 40, 64), 1.0, "bf16")
+    k = synth.normal(121, (2, 3, 40, 64), 1.0, "bf16")
+    v = synth.normal(122, (2, 3, 40, 64), 1.0, "bf16")
+    o1, l1 = oracle.attention(q, k, v, causal=True, nthreads=1, with_lse=True)
+    o4, l4 = oracle.attention(q, k, v, causal=True, nthreads=4, with_lse=True)
+    assert np.array_equal(o1, o4) and np.array_equal(l1, l4)
+    rows = np.array([0, 5, 39, 40, 119, 239])
+    orows, lrows = oracle.attention_rows(q, k, v, rows, causal=True, with_lse=True)
+    assert np.array_equal(orows, o1.reshape(-1, 64)[rows])
+    assert np.array_equal(lrows, l1.reshape(-1)[rows])
+
+
+def test_rejects_bad_problems():
+    q = np.zeros((1, 1, 4, 8), np.float32)
+    k = np.zeros((1, 1, 3, 8), np.float32)
+    with pytest.raises(ValueError):
+        oracle.attention(q, k, k, causal=True)              # causal with Nq > Nk
+    with pytest.raises(ValueError):
+        oracle.attention(q, np.zeros((1, 1, 0, 8), np.float32), np.zeros((1, 1, 0, 8), np.float32))
+    with pytest.raises(ValueError):
+        oracle.attention_rows(q, k, k, [12])               # row out of range
