@@ -1,0 +1,212 @@
+"""Benchmark of the fused attention hot path on one MI355X.
+
+One step = one call of the library on one batch of seeded synthetic input,
+already resident in device memory.  The default run times
+
+  * prefill (the main line): causal attention B=1, H=32, Nq=Nk=16384,
+    dk=dv=128, bf16 Q/K ~ N(0, 3^2), V ~ N(0, 1) -- one launch of the fused
+    MFMA tile kernel per step;
+  * decode (reported in the same line under "decode"): B=64, H=32, Nq=1,
+    Nk=8192, dk=dv=128, bf16 -- split-K kernel + combine kernel per step;
+
+each with HIP events on the stream the kernels run on, and reports achieved
+TFLOP/s (prefill, matrix-core bound) and GB/s (decode, HBM bound) against the
+MI355X peaks.  The fp64 CPU oracle is timed on a bounded sample of the
+prefill workload on the host's cores as a reported baseline.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--no-cpu-baseline] [--no-decode]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused attention TFLOP/s + HBM GB/s vs MI355X roofline, bf16 d=128"
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 matrix-core peak, TFLOP/s
+PEAK_HBM_GBS = 8000.0          # HBM3E peak, GB/s
+DEFAULT_PREFILL = "causal_long_b1h32_n16384_d128_bf16_qk_sigma3"
+DEFAULT_DECODE = "decode_b64h32_nk8192_d128_bf16"
+
+
+def visible_pairs(w) -> int:
+    """(query, key) pairs left visible by the mask: key j <= i + (Nk - Nq) when causal."""
+    if not w.causal:
+        return w.B * w.H * w.Nq * w.Nk
+    off = w.Nk - w.Nq
+    per_head = sum(min(w.Nk, i + off + 1) for i in range(w.Nq))
+    return w.B * w.H * per_head
+
+
+def algorithmic_flops(w) -> float:
+    """Matrix-product flops over visible pairs: 2*dk for Q.K^T plus 2*dv for P.V."""
+    return 2.0 * (w.dk + w.dv) * visible_pairs(w)
+
+
+def compulsory_bytes(w, out_bytes: int) -> int:
+    """Q, K and V read once, O written once."""
+    es = 4 if w.dtype == "f32" else 2
+    return w.B * w.H * ((w.Nq * w.dk + w.Nk * (w.dk + w.dv)) * es + w.Nq * w.dv * out_bytes)
+
+
+def _inputs(w, dev):
+    import synth
+    q, k, v = synth.make_inputs(w)
+    return (q, k, v), tuple(synth.to_torch(a, dev) for a in (q, k, v))
+
+
+def time_calls(fn, steps: int, warmup: int, stream):
+    """Average ms per call over `steps` calls, HIP events on `stream`."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def cpu_baseline(w, host_inputs, target_s: float = 12.0):
+    """Oracle on a bounded random sample of the workload's query rows."""
+    import numpy as np
+    import oracle
+    q, k, v = host_inputs
+    threads = len(os.sched_getaffinity(0))
+    rng = np.random.default_rng(0)
+    total = w.B * w.H * w.Nq
+
+    def flops_of(rows):
+        if not w.causal:
+            return 2.0 * (w.dk + w.dv) * w.Nk * rows.size
+        i = rows % w.Nq
+        return 2.0 * (w.dk + w.dv) * float(np.minimum(w.Nk, i + (w.Nk - w.Nq) + 1).sum())
+
+    probe = rng.integers(0, total, size=min(total, 64 * threads)).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.attention_rows(q, k, v, probe, scale=w.scale, causal=w.causal, nthreads=threads)
+    dt = time.perf_counter() - t0
+    n = int(min(total, max(probe.size, probe.size * target_s / max(dt, 1e-3))))
+    rows = rng.integers(0, total, size=n).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.attention_rows(q, k, v, rows, scale=w.scale, causal=w.causal, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {
+        "value": flops_of(rows) / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{rows.size} random query rows of {w.name} (of {total}), fp64, "
+                  f"{dt:.1f} s on {threads} OpenMP threads",
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_PREFILL)
+    ap.add_argument("--decode-workload", default=DEFAULT_DECODE)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--out-dtype", choices=["bf16", "f32"], default=None,
+                    help="output storage (default: the input storage type)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py: this library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(every (batch, head) slice is independent: larger jobs shard over GPUs "
+              "by slice with no communication, which one GPU's figure already measures).",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    import paper_2606_07713_amd as moa
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def run_workload(name):
+        w = synth.WORKLOADS[name]
+        host, (tq, tk, tv) = _inputs(w, dev)
+        odt = {"bf16": torch.bfloat16, "f32": torch.float32}[args.out_dtype or w.dtype]
+        out = torch.empty((w.B, w.H, w.Nq, w.dv), dtype=odt, device=dev)
+        ws_bytes = moa.moa_attn_workspace_bytes(w.B, w.H, w.Nq, w.Nk, w.dk, w.dv, 0)
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+
+        def call():
+            moa.attn_fwd(tq, tk, tv, scale=w.scale, causal=w.causal, out_dtype=odt, out=out,
+                         workspace=ws if ws_bytes else None, stream=stream)
+        ms = time_calls(call, args.steps, args.warmup, stream)
+        return w, host, ms, out.element_size()
+
+    w, host, ms, ob = run_workload(args.workload)
+    flops = algorithmic_flops(w)
+    tflops = flops / (ms * 1e-3) / 1e12
+    nbytes = compulsory_bytes(w, ob)
+    mfma_bound = flops / nbytes > PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if mfma_bound:
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": None}
+    else:
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None}
+    line = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "Nq": w.Nq, "Nk": w.Nk, "dk": w.dk,
+                   "dv": w.dv, "causal": w.causal, "in": w.dtype,
+                   "out": args.out_dtype or w.dtype, "flop_per_step": flops,
+                   "compulsory_bytes_per_step": nbytes,
+                   "hbm_GBps_compulsory": round(nbytes / (ms * 1e-3) / 1e9, 1)},
+        "roofline": roof,
+    }
+    print(f"# prefill {w.name}: {ms:.4f} ms/step, {tflops:.1f} TFLOP/s", file=sys.stderr, flush=True)
+
+    if not args.no_decode:
+        wd, _, msd, obd = run_workload(args.decode_workload)
+        bd = compulsory_bytes(wd, obd)
+        gbs = bd / (msd * 1e-3) / 1e9
+        line["decode"] = {
+            "workload": wd.name, "ms_per_call": round(msd, 4),
+            "splits": moa.moa_attn_num_splits(wd.B, wd.H, wd.Nq, wd.Nk, wd.dk, wd.dv, 0),
+            "value": round(gbs, 1), "unit": "GB/s",
+            "tflops": round(algorithmic_flops(wd) / (msd * 1e-3) / 1e12, 2),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
+        print(f"# decode {wd.name}: {msd:.4f} ms/call, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
+
+    line["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(w, host)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,137 @@
+/*
+ * moa_attn.h -- C ABI of the fused scaled dot-product attention library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the paper's problem statement (Sec. "MoA DNF Derivation of
+ * Attention", eq. attention with the stable softmax of eq. stable_softmax),
+ * applied independently to every (batch, head) slice as the remark on
+ * higher-rank tensors in that section prescribes:
+ *
+ *   O[b,h,i,:] = sum_j P[b,h,i,j] * V[b,h,j,:]
+ *   P[b,h,i,:] = softmax over visible j of  scale * <Q[b,h,i,:], K[b,h,j,:]>
+ *
+ * computed as in the Denotational Normal Form (eqs. dnf_attn, output_dnf):
+ * no transposed-K buffer, no score matrix and no softmax temporary is ever
+ * written to device memory.  The only device-memory writes of a prefill call
+ * are O (and LSE when requested); a decode call (Nq == 1) additionally writes
+ * per-split partial results of size O(B*H*splits*dv) into the caller's
+ * workspace.
+ *
+ * Conventions shared by all entry points
+ *  - Plain C types only; no HIP or framework types appear here.  `stream` is a
+ *    hipStream_t passed as void* (NULL = the default stream).
+ *  - All tensor pointers are DEVICE pointers owned by the caller, contiguous,
+ *    row-major (last index fastest; the paper's gamma layout):
+ *      Q [B][H][Nq][dk]   K [B][H][Nk][dk]   V [B][H][Nk][dv]   O [B][H][Nq][dv]
+ *      LSE [B][H][Nq] fp32 (optional, NULL = not written)
+ *    Every tensor pointer must be 16-byte aligned.
+ *  - The library allocates no device memory, keeps no state between calls,
+ *    never synchronises, and is safe to call from several host threads.  Work
+ *    is enqueued on `stream` (at most two kernels); errors raised by kernels
+ *    surface at the caller's next synchronisation.
+ *  - Arguments are validated on the host before any HIP call; a rejected call
+ *    touches no device memory.
+ */
+#ifndef MOA_ATTN_H
+#define MOA_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+enum {
+    MOA_OK = 0,
+    MOA_ERR_INVALID_ARG = 1,  /* NULL pointer, bad dimension, misaligned or overlapping buffers,
+                                 non-finite scale, causal with Nq > Nk, unknown dtype */
+    MOA_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement (head size) */
+    MOA_ERR_WORKSPACE = 3,    /* workspace missing or smaller than moa_attn_workspace_bytes() */
+    MOA_ERR_HIP = 4           /* the HIP runtime reported an error while enqueueing */
+};
+
+/* Storage types for Q, K, V (in_dtype) and O (out_dtype). */
+enum {
+    MOA_F32 = 0,   /* IEEE binary32 */
+    MOA_BF16 = 1   /* bfloat16 (upper half of binary32) */
+};
+
+/*
+ * moa_attn_workspace_bytes -- device workspace a moa_attn_fwd call with the
+ * same arguments needs, in bytes (0 when none).
+ *
+ * Only decode-shaped calls (Nq == 1) need a workspace: they split the key
+ * range into `num_splits` chunks (0 = the library's choice, which this
+ * function then reports for) and combine the partial softmax results in a
+ * second pass; the workspace holds those partials, fp32, for B*H*splits rows.
+ * Returns 0 for prefill-shaped calls and for invalid dimensions.
+ */
+size_t moa_attn_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
+                                int64_t dv, int num_splits);
+
+/*
+ * moa_attn_num_splits -- the number of key splits a decode-shaped call
+ * (Nq == 1) with these arguments will use (1 for prefill-shaped calls).
+ */
+int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                        int num_splits);
+
+/*
+ * moa_attn_fwd -- fused attention forward (eq. attention; DNF eqs. dnf_attn
+ * and output_dnf; the max-subtracted softmax of eq. stable_softmax).
+ *
+ * Q, K, V   device inputs of storage type in_dtype (MOA_F32 or MOA_BF16, the
+ *           same for all three), layouts above.
+ * O         device output of storage type out_dtype (MOA_F32, or in_dtype).
+ * LSE       optional device output, fp32 [B][H][Nq]: the natural log of the
+ *           softmax denominator, LSE = max_j s_j + ln(sum_j exp(s_j - max_j s_j))
+ *           with s_j = scale * <q, k_j> over visible j.  NULL = not written.
+ * B, H      batch and head counts (>= 0).
+ * Nq, Nk    query and key counts (Nq >= 0, Nk >= 1).
+ * dk, dv    head sizes; supported: dk == dv in {64, 128}.
+ * scale     finite fp32 multiplier of the inner products (the paper divides
+ *           by sqrt(dk): pass 1/sqrt(dk) for that).  0 and negative values
+ *           are valid.
+ * causal    0: every key is visible.  1: key j is visible to query i iff
+ *           j <= i + (Nk - Nq) (bottom-right aligned; j <= i when Nq == Nk).
+ *           Requires Nq <= Nk, so no query row is fully masked.
+ * workspace, workspace_bytes
+ *           device scratch for decode-shaped calls; at least
+ *           moa_attn_workspace_bytes(...) bytes, 16-byte aligned, not
+ *           overlapping any tensor.  May be NULL/0 when that is 0.
+ * num_splits
+ *           decode key splits (0 = library's choice, else 1..256).
+ * stream    hipStream_t as void*.
+ *
+ * Computation: inner products and softmax statistics in fp32 from exact
+ * products of the inputs; bf16 inputs use bf16 matrix-core products with fp32
+ * accumulation and the unnormalised weights rounded to bf16 before they
+ * multiply V.  Results are deterministic: identical inputs give bit-identical
+ * outputs (no atomics).
+ *
+ * Returns MOA_OK once the work is enqueued (or when B*H*Nq == 0: nothing is
+ * launched), else one of the MOA_ERR_* codes above.
+ */
+int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE, int64_t B,
+                 int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale, int causal,
+                 int in_dtype, int out_dtype, void* workspace, size_t workspace_bytes,
+                 int num_splits, void* stream);
+
+/* moa_attn_status_string -- static, human-readable text for a status code. */
+const char* moa_attn_status_string(int status);
+
+/*
+ * moa_attn_last_hip_error -- name of the HIP runtime error (e.g.
+ * "hipErrorInvalidDeviceFunction") behind the most recent MOA_ERR_HIP
+ * returned on the calling thread; "hipSuccess" if there was none.  Static
+ * string, never NULL.
+ */
+const char* moa_attn_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOA_ATTN_H */

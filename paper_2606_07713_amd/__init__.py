@@ -1,0 +1,148 @@
+"""Fused scaled dot-product attention for AMD Instinct MI355X (gfx950).
+
+A thin binding over ``libmoa_attn.so``, whose C ABI is ``include/moa_attn.h``.
+The Python names mirror the C entry points (``moa_attn_fwd``,
+``moa_attn_workspace_bytes``, ``moa_attn_num_splits``,
+``moa_attn_status_string``) and only marshal arguments; every step of the
+computation runs in the library's HIP kernels.  ``attn_fwd`` is a convenience
+wrapper for torch tensors (torch supplies device memory and the stream).
+
+There is no fallback: if the HIP library has not been built, importing this
+package raises ``ImportError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+__all__ = [
+    "MOA_OK", "MOA_ERR_INVALID_ARG", "MOA_ERR_UNSUPPORTED", "MOA_ERR_WORKSPACE", "MOA_ERR_HIP",
+    "MOA_F32", "MOA_BF16", "MoaAttnError", "moa_attn_fwd", "moa_attn_workspace_bytes",
+    "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd", "LIB_PATH", "lib",
+]
+
+MOA_OK, MOA_ERR_INVALID_ARG, MOA_ERR_UNSUPPORTED, MOA_ERR_WORKSPACE, MOA_ERR_HIP = 0, 1, 2, 3, 4
+MOA_F32, MOA_BF16 = 0, 1
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoa_attn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: the HIP attention library has not been built "
+        "(run `python paper_2606_07713_amd/build.py` or __graft_entry__.build()).")
+
+# torch ships its own HIP runtime under the same soname as ROCm's.  Whichever
+# is loaded first serves the whole process, so load torch's before the library
+# resolves its HIP dependency: two runtimes in one process cannot share a GPU
+# (kernels enqueued through the second one fail with hipErrorNoDevice).
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:  # plain C-ABI use without torch: ROCm's runtime is used
+    _torch = None
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_i64, _vp, _f32, _ci, _sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_int, ctypes.c_size_t
+lib.moa_attn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _f32,
+                             _ci, _ci, _ci, _vp, _sz, _ci, _vp]
+lib.moa_attn_fwd.restype = _ci
+lib.moa_attn_workspace_bytes.argtypes = [_i64] * 6 + [_ci]
+lib.moa_attn_workspace_bytes.restype = _sz
+lib.moa_attn_num_splits.argtypes = [_i64] * 6 + [_ci]
+lib.moa_attn_num_splits.restype = _ci
+lib.moa_attn_status_string.argtypes = [_ci]
+lib.moa_attn_status_string.restype = ctypes.c_char_p
+lib.moa_attn_last_hip_error.argtypes = []
+lib.moa_attn_last_hip_error.restype = ctypes.c_char_p
+
+
+class MoaAttnError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        msg = f"moa_attn_fwd failed: {moa_attn_status_string(status)} (status {status})"
+        if status == MOA_ERR_HIP:
+            msg += f": {moa_attn_last_hip_error()}"
+        super().__init__(msg)
+
+
+def moa_attn_status_string(status: int) -> str:
+    return lib.moa_attn_status_string(int(status)).decode()
+
+
+def moa_attn_last_hip_error() -> str:
+    return lib.moa_attn_last_hip_error().decode()
+
+
+def moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits=0) -> int:
+    return int(lib.moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits))
+
+
+def moa_attn_num_splits(B, H, Nq, Nk, dk, dv, num_splits=0) -> int:
+    return int(lib.moa_attn_num_splits(B, H, Nq, Nk, dk, dv, num_splits))
+
+
+def moa_attn_fwd(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, scale, causal, in_dtype, out_dtype,
+                 workspace, workspace_bytes, num_splits, stream) -> int:
+    """Raw C call: pointers are ints (device addresses) or None; returns the status."""
+    return int(lib.moa_attn_fwd(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, float(scale), int(causal),
+                                in_dtype, out_dtype, workspace, workspace_bytes, num_splits,
+                                stream))
+
+
+def _dtype_code(t):
+    import torch
+    if t == torch.float32:
+        return MOA_F32
+    if t == torch.bfloat16:
+        return MOA_BF16
+    raise TypeError(f"unsupported dtype {t}; use torch.float32 or torch.bfloat16")
+
+
+def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False,
+             num_splits=0, out=None, workspace=None, stream=None):
+    """Fused attention on torch device tensors [B, H, N, d] (contiguous, same dtype).
+
+    Returns O [B, H, Nq, dv] (and LSE [B, H, Nq] fp32 when ``return_lse``).
+    ``scale`` defaults to 1/sqrt(dk).  Raises ``MoaAttnError`` on a rejected call.
+    """
+    import torch
+    if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
+        raise ValueError("q, k, v must be [B, H, N, d]")
+    for t in (q, k, v):
+        if not t.is_cuda:
+            raise ValueError("q, k, v must be device tensors")
+        if not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share one dtype")
+    B, H, Nq, dk = q.shape
+    Nk, dv = k.shape[2], v.shape[3]
+    if tuple(k.shape) != (B, H, Nk, dk) or tuple(v.shape) != (B, H, Nk, dv):
+        raise ValueError(f"shape mismatch {tuple(q.shape)} {tuple(k.shape)} {tuple(v.shape)}")
+    in_code = _dtype_code(q.dtype)
+    odt = q.dtype if out_dtype is None else out_dtype
+    out_code = _dtype_code(odt)
+    if scale is None:
+        scale = 1.0 / math.sqrt(dk)
+    if out is None:
+        out = torch.empty((B, H, Nq, dv), dtype=odt, device=q.device)
+    elif (tuple(out.shape) != (B, H, Nq, dv) or out.dtype != odt or not out.is_contiguous()
+          or out.device != q.device):
+        raise ValueError("out must be a contiguous [B, H, Nq, dv] tensor of the output dtype")
+    lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device) if return_lse else None
+    ws_bytes = moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    st = moa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                      lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv, scale,
+                      causal, in_code, out_code,
+                      workspace.data_ptr() if workspace is not None else None,
+                      workspace.numel() * workspace.element_size() if workspace is not None else 0,
+                      num_splits,
+                      stream.cuda_stream)
+    if st != MOA_OK:
+        raise MoaAttnError(st)
+    return (out, lse) if return_lse else out

@@ -1,0 +1,167 @@
+// C-ABI front end of the attention library: argument validation, workspace
+// sizing and kernel dispatch.  Everything here is host code; it allocates no
+// device memory and never synchronises.
+#include <cmath>
+#include <cstdint>
+#include <limits>
+
+#include "../../include/moa_attn.h"
+#include "launch.h"
+
+namespace {
+
+constexpr int kMaxSplits = 256;
+// Keys a decode workgroup should stream at least, and the workgroup count the
+// automatic split choice aims for (several waves of workgroups per CU).
+constexpr int64_t kMinKeysPerSplit = 256;
+constexpr int64_t kTargetDecodeBlocks = 8192;
+
+bool dims_ok(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv) {
+    return B >= 0 && H >= 0 && Nq >= 0 && Nk >= 1 && dk >= 1 && dv >= 1;
+}
+
+bool head_supported(int64_t dk, int64_t dv) { return dk == dv && (dk == 64 || dk == 128); }
+
+// In-head offsets are 32-bit in the kernels; grids are 1-D.
+bool sizes_fit(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d) {
+    const int64_t lim = std::numeric_limits<int32_t>::max();
+    if (Nq > lim / d || Nk > lim / d) return false;
+    if (B != 0 && H > lim / B) return false;
+    const int64_t bh = B * H;
+    const int64_t qtiles = (Nq + moa::kPrefillF32RowsPerBlock - 1) / moa::kPrefillF32RowsPerBlock;
+    if (bh != 0 && qtiles > lim / bh) return false;
+    if (bh != 0 && kMaxSplits > lim / bh) return false;
+    return true;
+}
+
+int pick_splits(int64_t bh, int64_t Nk, int requested) {
+    if (requested > 0) return requested;
+    int64_t s = (kTargetDecodeBlocks + bh - 1) / (bh > 0 ? bh : 1);
+    const int64_t cap = (Nk + kMinKeysPerSplit - 1) / kMinKeysPerSplit;
+    if (s > cap) s = cap;
+    if (s > kMaxSplits) s = kMaxSplits;
+    if (s < 1) s = 1;
+    return (int)s;
+}
+
+// Name of the HIP error behind the last MOA_ERR_HIP returned on this thread.
+thread_local const char* g_last_hip_error = "hipSuccess";
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t decode_ws_bytes(int64_t bh, int64_t d, int splits) {
+    return align256((size_t)bh * (size_t)splits * (size_t)(d + 2) * sizeof(float));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+    if (an == 0 || bn == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                        int num_splits) {
+    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq != 1) return 1;
+    if (num_splits < 0 || num_splits > kMaxSplits) return 1;
+    return pick_splits(B * H, Nk, num_splits);
+}
+
+size_t moa_attn_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
+                                int64_t dv, int num_splits) {
+    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq != 1) return 0;
+    if (num_splits < 0 || num_splits > kMaxSplits) return 0;
+    if (!head_supported(dk, dv) || !sizes_fit(B, H, Nq, Nk, dk)) return 0;
+    const int64_t bh = B * H;
+    if (bh == 0) return 0;
+    return decode_ws_bytes(bh, dk, pick_splits(bh, Nk, num_splits));
+}
+
+int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE, int64_t B,
+                 int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale,
+                 int causal, int in_dtype, int out_dtype, void* workspace,
+                 size_t workspace_bytes, int num_splits, void* stream) {
+    // ---- validation: no HIP call happens before all of it has passed
+    if (!Q || !K || !V || !O) return MOA_ERR_INVALID_ARG;
+    if (!dims_ok(B, H, Nq, Nk, dk, dv)) return MOA_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return MOA_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1) return MOA_ERR_INVALID_ARG;
+    if (causal && Nq > Nk) return MOA_ERR_INVALID_ARG;
+    if (in_dtype != MOA_F32 && in_dtype != MOA_BF16) return MOA_ERR_INVALID_ARG;
+    if (out_dtype != MOA_F32 && out_dtype != in_dtype) return MOA_ERR_INVALID_ARG;
+    if (num_splits < 0 || num_splits > kMaxSplits) return MOA_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) ||
+        (LSE && !aligned16(LSE)) || (workspace && !aligned16(workspace)))
+        return MOA_ERR_INVALID_ARG;
+    if (!head_supported(dk, dv)) return MOA_ERR_UNSUPPORTED;
+    if (!sizes_fit(B, H, Nq, Nk, dk)) return MOA_ERR_UNSUPPORTED;
+
+    const int64_t bh = B * H;
+    const size_t ies = in_dtype == MOA_F32 ? 4 : 2;
+    const size_t oes = out_dtype == MOA_F32 ? 4 : 2;
+    const size_t qn = (size_t)bh * Nq * dk * ies, kn = (size_t)bh * Nk * dk * ies;
+    const size_t vn = (size_t)bh * Nk * dv * ies, on = (size_t)bh * Nq * dv * oes;
+    const size_t ln = LSE ? (size_t)bh * Nq * sizeof(float) : 0;
+    if (overlaps(O, on, Q, qn) || overlaps(O, on, K, kn) || overlaps(O, on, V, vn))
+        return MOA_ERR_INVALID_ARG;
+    if (LSE && (overlaps(LSE, ln, O, on) || overlaps(LSE, ln, Q, qn) ||
+                overlaps(LSE, ln, K, kn) || overlaps(LSE, ln, V, vn)))
+        return MOA_ERR_INVALID_ARG;
+
+    const bool decode = (Nq == 1);
+    int splits = 1;
+    size_t need = 0;
+    if (decode && bh > 0) {
+        splits = pick_splits(bh, Nk, num_splits);
+        need = decode_ws_bytes(bh, dk, splits);
+        if (!workspace || workspace_bytes < need) return MOA_ERR_WORKSPACE;
+        const size_t wn = need;
+        if (overlaps(workspace, wn, O, on) || overlaps(workspace, wn, Q, qn) ||
+            overlaps(workspace, wn, K, kn) || overlaps(workspace, wn, V, vn) ||
+            (LSE && overlaps(workspace, wn, LSE, ln)))
+            return MOA_ERR_INVALID_ARG;
+    }
+    if (bh == 0 || Nq == 0) return MOA_OK;
+
+    moa::Problem p;
+    p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
+    p.bh = (int)bh; p.nq = (int)Nq; p.nk = (int)Nk; p.d = (int)dk;
+    p.scale = scale;
+    p.causal = causal != 0;
+    p.in_bf16 = in_dtype == MOA_BF16;
+    p.out_bf16 = out_dtype == MOA_BF16;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    hipError_t e;
+    if (decode)
+        e = moa::launch_decode(p, splits, static_cast<float*>(workspace), s);
+    else if (p.in_bf16)
+        e = moa::launch_prefill_bf16(p, s);
+    else
+        e = moa::launch_prefill_f32(p, s);
+    if (e != hipSuccess) {
+        g_last_hip_error = hipGetErrorName(e);
+        return MOA_ERR_HIP;
+    }
+    return MOA_OK;
+}
+
+const char* moa_attn_last_hip_error(void) { return g_last_hip_error; }
+
+const char* moa_attn_status_string(int status) {
+    switch (status) {
+        case MOA_OK: return "ok";
+        case MOA_ERR_INVALID_ARG: return "invalid argument";
+        case MOA_ERR_UNSUPPORTED: return "unsupported head size or problem size";
+        case MOA_ERR_WORKSPACE: return "workspace missing or too small";
+        case MOA_ERR_HIP: return "HIP runtime error while enqueueing";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

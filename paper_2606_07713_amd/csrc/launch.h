@@ -1,0 +1,42 @@
+// Internal launch interface between the C-ABI front end (api.cpp) and the
+// kernels.  Not installed; the public interface is include/moa_attn.h.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace moa {
+
+// One fused-attention problem after validation.  Pointers are device
+// pointers; sizes are already checked to fit the kernels' 32-bit in-head
+// offsets.
+struct Problem {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    float* lse;        // nullable
+    int bh;            // B*H
+    int nq, nk, d;     // d = dk = dv
+    float scale;
+    bool causal;
+    bool in_bf16;
+    bool out_bf16;
+};
+
+// Prefill, bf16 inputs: one launch of the MFMA tile kernel.
+hipError_t launch_prefill_bf16(const Problem& p, hipStream_t stream);
+
+// Prefill, fp32 inputs: one launch of the fp32 vector-ALU tile kernel.
+hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream);
+
+// Decode (Nq == 1): split-K partial kernel + combine kernel.
+// `ws` holds bh*splits*(d + 2) floats.
+hipError_t launch_decode(const Problem& p, int splits, float* ws, hipStream_t stream);
+
+// Row-tile size of the bf16 prefill kernel (queries per workgroup).
+constexpr int kPrefillBf16RowsPerBlock = 128;
+// Row-tile size of the fp32 prefill kernel.
+constexpr int kPrefillF32RowsPerBlock = 64;
+
+}  // namespace moa

@@ -1,0 +1,150 @@
+// Fused attention prefill for fp32 inputs and fp32 output (vector ALU, fp32
+// throughout).
+//
+// Used where the inputs are fp32 and the result must stay within fp32
+// rounding of the exact attention (no bf16 rounding of any operand).  One
+// workgroup owns 64 queries of one (batch*head); each query row is handled by
+// a quad of 4 lanes that split d, and K/V tiles of 32 keys are staged in LDS
+// and read by all quads as broadcasts.  Scores, the running max and sum and
+// the exponentials stay in registers (DNF eqs. dnf_attn / output_dnf); only O
+// (and optional LSE) are written.
+#include "device_common.h"
+#include "launch.h"
+
+namespace moa {
+namespace {
+
+constexpr int ROWS = 64;          // queries per workgroup
+constexpr int THREADS = ROWS * 4;
+constexpr int KT = 32;            // keys per tile
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
+    constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
+    __shared__ __attribute__((aligned(16))) float Ks[KT * D];
+    __shared__ __attribute__((aligned(16))) float Vs[KT * D];
+
+    const int tid = threadIdx.x;
+    const int quad = tid & 3;
+    const int bh = blockIdx.x / n_qtiles;
+    const int qt = blockIdx.x % n_qtiles;
+    const int qrow = qt * ROWS + (tid >> 2);
+    const int qrow_c = qrow < Nq ? qrow : Nq - 1;
+    const int off = Nk - Nq;
+
+    const float* Qh = Q + (size_t)bh * Nq * D;
+    const float* Kh = K + (size_t)bh * Nk * D;
+    const float* Vh = V + (size_t)bh * Nk * D;
+
+    float4 qv[CH], acc[CH];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        qv[j] = *reinterpret_cast<const float4*>(Qh + (size_t)qrow_c * D + (j * 4 + quad) * 4);
+        acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    float m_run = kNegInf, l_run = 0.0f;
+
+    int kv_end = Nk;
+    if (CAUSAL) kv_end = min(Nk, qt * ROWS + ROWS + off);
+    const int n_kt = (kv_end + KT - 1) / KT;
+
+    for (int kt = 0; kt < n_kt; ++kt) {
+        const int kbase = kt * KT;
+        __syncthreads();
+        for (int idx = tid; idx < KT * D / 4; idx += THREADS) {
+            const int row = idx / (D / 4), ch = idx % (D / 4);
+            const int key = min(kbase + row, Nk - 1);
+            *reinterpret_cast<float4*>(&Ks[row * D + ch * 4]) =
+                *reinterpret_cast<const float4*>(Kh + (size_t)key * D + ch * 4);
+            *reinterpret_cast<float4*>(&Vs[row * D + ch * 4]) =
+                *reinterpret_cast<const float4*>(Vh + (size_t)key * D + ch * 4);
+        }
+        __syncthreads();
+
+        // scores of this tile, in log2 units (t = c * <q, k>)
+        float t[KT];
+        float tmax = kNegInf;
+#pragma unroll
+        for (int j = 0; j < KT; ++j) {
+            float part = 0.0f;
+#pragma unroll
+            for (int h = 0; h < CH; ++h) {
+                const float4 kk = *reinterpret_cast<const float4*>(&Ks[j * D + (h * 4 + quad) * 4]);
+                part = __builtin_fmaf(qv[h].x, kk.x, part);
+                part = __builtin_fmaf(qv[h].y, kk.y, part);
+                part = __builtin_fmaf(qv[h].z, kk.z, part);
+                part = __builtin_fmaf(qv[h].w, kk.w, part);
+            }
+            const float s = group_sum<4>(part);
+            const int key = kbase + j;
+            const bool vis = key < Nk && (!CAUSAL || key <= qrow + off);
+            t[j] = vis ? s * c : kNegInf;
+            tmax = fmaxf(tmax, t[j]);
+        }
+        const float m_new = fmaxf(m_run, tmax);
+        if (m_new != kNegInf) {
+            const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int h = 0; h < CH; ++h) {
+                acc[h].x *= alpha; acc[h].y *= alpha; acc[h].z *= alpha; acc[h].w *= alpha;
+            }
+            m_run = m_new;
+        }
+#pragma unroll
+        for (int j = 0; j < KT; ++j) {
+            const float p = (t[j] == kNegInf) ? 0.0f : exp2_hw(t[j] - m_run);
+            l_run += p;
+#pragma unroll
+            for (int h = 0; h < CH; ++h) {
+                const float4 vv = *reinterpret_cast<const float4*>(&Vs[j * D + (h * 4 + quad) * 4]);
+                acc[h].x = __builtin_fmaf(p, vv.x, acc[h].x);
+                acc[h].y = __builtin_fmaf(p, vv.y, acc[h].y);
+                acc[h].z = __builtin_fmaf(p, vv.z, acc[h].z);
+                acc[h].w = __builtin_fmaf(p, vv.w, acc[h].w);
+            }
+        }
+    }
+
+    if (qrow < Nq) {
+        const float inv = 1.0f / l_run;
+        const size_t obase = ((size_t)bh * Nq + qrow) * D;
+#pragma unroll
+        for (int h = 0; h < CH; ++h) {
+            const int d0 = (h * 4 + quad) * 4;
+            const float4 o = make_float4(acc[h].x * inv, acc[h].y * inv, acc[h].z * inv, acc[h].w * inv);
+            *reinterpret_cast<float4*>(Out + obase + d0) = o;
+        }
+        if (LSE != nullptr && quad == 0)
+            LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_run)) * kLn2;
+    }
+}
+
+template <int D, bool CAUSAL>
+hipError_t launch(const Problem& p, hipStream_t stream) {
+    const int n_qtiles = (p.nq + ROWS - 1) / ROWS;
+    const long long blocks = (long long)p.bh * n_qtiles;
+    return launch_kernel(prefill_f32_kernel<D, CAUSAL>, dim3((unsigned)blocks), dim3(THREADS),
+                         stream, static_cast<const float*>(p.q), static_cast<const float*>(p.k),
+                         static_cast<const float*>(p.v), static_cast<float*>(p.o), p.lse, p.nq,
+                         p.nk, n_qtiles, p.scale * kLog2e);
+}
+
+template <int D>
+hipError_t launch_d(const Problem& p, hipStream_t stream) {
+    return p.causal ? launch<D, true>(p, stream) : launch<D, false>(p, stream);
+}
+
+}  // namespace
+
+static_assert(ROWS == kPrefillF32RowsPerBlock, "row tile mismatch");
+
+hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream) {
+    if (p.d == 64) return launch_d<64>(p, stream);
+    if (p.d == 128) return launch_d<128>(p, stream);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace moa

@@ -1,0 +1,120 @@
+"""The C-ABI library on the CPU: it loads, exports what its header declares,
+and rejects invalid calls before touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moa_attn.h")
+
+moa = pytest.importorskip("paper_2606_07713_amd", reason="HIP library not built")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moa_attn_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared_functions()
+    assert names == ["moa_attn_fwd", "moa_attn_last_hip_error", "moa_attn_num_splits",
+                     "moa_attn_status_string", "moa_attn_workspace_bytes"]
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(moa.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+        assert hasattr(moa, name), f"python binding lacks {name}"
+
+
+def test_header_is_plain_c():
+    # The header must compile as C with no HIP include path.
+    import subprocess
+    import tempfile
+    src = '#include "moa_attn.h"\nint main(void){return MOA_OK;}\n'
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "t.c")
+        open(c, "w").write(src)
+        r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER),
+                            c, "-o", os.path.join(d, "t")], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
+def test_status_strings():
+    assert moa.moa_attn_status_string(moa.MOA_OK) == "ok"
+    for s in (1, 2, 3, 4):
+        assert moa.moa_attn_status_string(s) not in ("ok", "unknown status")
+    assert moa.moa_attn_status_string(99) == "unknown status"
+    assert moa.moa_attn_last_hip_error() == "hipSuccess"
+
+
+def test_workspace_and_splits():
+    # prefill-shaped calls need no workspace
+    assert moa.moa_attn_workspace_bytes(2, 16, 4096, 4096, 128, 128, 0) == 0
+    assert moa.moa_attn_num_splits(2, 16, 4096, 4096, 128, 128, 0) == 1
+    # decode: partials of bh*splits rows of (d + 2) floats, rounded up to 256 B
+    s = moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 0)
+    assert 1 <= s <= 256
+    ws = moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 0)
+    assert ws >= 64 * 32 * s * 130 * 4 and ws % 256 == 0
+    assert moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 5) == 5
+    assert moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 5) >= 64 * 32 * 5 * 130 * 4
+    # short key ranges are not split below the minimum chunk
+    assert moa.moa_attn_num_splits(1, 1, 1, 100, 64, 64, 0) == 1
+    assert moa.moa_attn_workspace_bytes(1, 1, 1, 8192, 96, 96, 0) == 0   # unsupported head
+
+
+# Fake, 16-byte-aligned, non-overlapping "device" addresses: validation must
+# reject every call below before it dereferences or launches anything.
+A, BUF, C, D, W = 1 << 40, 2 << 40, 3 << 40, 4 << 40, 5 << 40
+
+
+def _call(**kw):
+    args = dict(Q=A, K=BUF, V=C, O=D, LSE=None, B=1, H=1, Nq=8, Nk=8, dk=64, dv=64, scale=0.125,
+                causal=0, in_dtype=moa.MOA_BF16, out_dtype=moa.MOA_BF16, workspace=None,
+                workspace_bytes=0, num_splits=0, stream=None)
+    args.update(kw)
+    return moa.moa_attn_fwd(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Q=None), 1), (dict(K=None), 1), (dict(V=None), 1), (dict(O=None), 1),
+    (dict(B=-1), 1), (dict(H=-1), 1), (dict(Nq=-1), 1), (dict(Nk=0), 1), (dict(dk=0), 1),
+    (dict(scale=float("nan")), 1), (dict(scale=float("inf")), 1),
+    (dict(causal=1, Nq=9, Nk=8), 1), (dict(causal=2), 1),
+    (dict(in_dtype=7), 1), (dict(out_dtype=7), 1),
+    (dict(in_dtype=0, out_dtype=1), 1),                # fp32 in, bf16 out is not offered
+    (dict(Q=A + 2), 1), (dict(O=D + 8), 1), (dict(LSE=D + 4), 1),
+    (dict(O=A + 64), 1),                               # O overlaps Q
+    (dict(num_splits=-1), 1), (dict(num_splits=257), 1),
+    (dict(dk=96, dv=96), 2), (dict(dk=64, dv=128), 2), (dict(dk=256, dv=256), 2),
+    (dict(Nq=1), 3),                                   # decode needs a workspace
+    (dict(Nq=1, workspace=W, workspace_bytes=16), 3),
+    (dict(Nq=1, workspace=A, workspace_bytes=1 << 20), 1),   # workspace overlaps Q
+])
+def test_validation_rejects_before_any_gpu_work(kw, status):
+    assert _call(**kw) == status
+
+
+def test_empty_problems_are_no_ops():
+    # Nothing to compute: returns OK without launching (no GPU needed).
+    assert _call(B=0) == moa.MOA_OK
+    assert _call(H=0) == moa.MOA_OK
+    assert _call(Nq=0) == moa.MOA_OK
+
+
+def test_one_hip_runtime_per_process():
+    # The binding must leave exactly one HIP runtime mapped (torch's, when torch
+    # is present), whatever was imported first.
+    import subprocess
+    import sys
+    code = ("import paper_2606_07713_amd, torch\n"
+            "paths = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(paths))\n")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1"

@@ -1,0 +1,137 @@
+"""Parity of the HIP path with the fp64 oracle on the same seeded inputs.
+
+Tolerances (max-abs, relative to std(V) = 1): 1e-5 for fp32 inputs, 2e-2 for
+bf16 inputs.  Small and ragged shapes are compared element by element; the
+full-size workloads run in the launch configuration the benchmark times and
+are checked on sampled rows the oracle computes one by one.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import TOL, gen, max_err, oracle_full, run_gpu, sample_rows, say
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def _seed(*parts):
+    return zlib.crc32(repr(parts).encode()) % 100003
+
+
+# ---------------------------------------------------------------- small shapes
+
+PREFILL_SHAPES = [
+    # B, H, Nq, Nk, d
+    (1, 1, 2, 2, 64),
+    (1, 2, 17, 17, 64),
+    (2, 2, 63, 65, 128),
+    (1, 3, 129, 127, 64),      # Nq > Nk (non-causal only)
+    (1, 2, 128, 128, 128),
+    (2, 1, 200, 1000, 128),    # Nq < Nk: causal is bottom-right aligned
+    (1, 1, 1000, 1000, 64),
+    (1, 2, 300, 300, 128),
+]
+
+
+@pytest.mark.parametrize("shape", PREFILL_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+@pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
+def test_prefill_matches_oracle(shape, causal, dtype, out_dtype):
+    B, H, Nq, Nk, d = shape
+    if causal and Nq > Nk:
+        pytest.skip("causal requires Nq <= Nk")
+    say(f"prefill {shape} causal={causal} {dtype}->{out_dtype}")
+    q, k, v = gen(B, H, Nq, Nk, d, dtype, seed=_seed(shape, causal, dtype))
+    o, lse = run_gpu(q, k, v, causal=causal, out_dtype=out_dtype, return_lse=True)
+    ref, ref_lse = oracle_full(q, k, v, causal=causal, with_lse=True)
+    err = max_err(o, ref)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL[dtype]
+    assert max_err(lse, ref_lse) <= (1e-5 if dtype == "f32" else 1e-4) * max(1.0, np.abs(ref_lse).max())
+
+
+DECODE_CASES = [
+    # B, H, Nk, d, splits
+    (1, 1, 1, 64, 0),
+    (2, 3, 7, 128, 0),
+    (2, 2, 100, 64, 3),
+    (3, 2, 1000, 128, 0),
+    (3, 2, 1000, 128, 16),
+    (1, 4, 8192, 128, 0),
+    (2, 2, 4097, 64, 5),
+]
+
+
+@pytest.mark.parametrize("case", DECODE_CASES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_decode_matches_oracle(case, dtype, out_dtype, causal):
+    B, H, Nk, d, splits = case
+    say(f"decode {case} {dtype}->{out_dtype} causal={causal}")
+    q, k, v = gen(B, H, 1, Nk, d, dtype, seed=_seed(case, dtype))
+    o, lse = run_gpu(q, k, v, causal=causal, out_dtype=out_dtype, num_splits=splits, return_lse=True)
+    ref, ref_lse = oracle_full(q, k, v, causal=causal, with_lse=True)
+    err = max_err(o, ref)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL[dtype]
+    assert max_err(lse, ref_lse) <= (1e-5 if dtype == "f32" else 1e-4) * max(1.0, np.abs(ref_lse).max())
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.125, 0.3])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("nq", [1, 77])
+def test_unusual_scales(scale, dtype, nq):
+    say(f"scale {scale} {dtype} nq={nq}")
+    q, k, v = gen(2, 2, nq, 150, 64, dtype, seed=17)
+    o = run_gpu(q, k, v, causal=True, scale=scale, out_dtype="f32")
+    ref = oracle_full(q, k, v, causal=True, scale=scale)
+    assert max_err(o, ref) <= TOL[dtype]
+
+
+# -------------------------------------------------------- full-size workloads
+
+def _check_workload(name, n_rows, out_dtype):
+    w = synth.WORKLOADS[name]
+    say(f"workload {name} -> {out_dtype}: generating inputs")
+    q, k, v = synth.make_inputs(w)
+    say("  running GPU")
+    o = run_gpu(q, k, v, causal=w.causal, scale=w.scale, out_dtype=out_dtype)
+    assert np.all(np.isfinite(o))
+    if n_rows is None:
+        say("  oracle (all rows)")
+        ref = oracle.attention(q, k, v, scale=w.scale, causal=w.causal)
+        err = max_err(o, ref)
+    else:
+        rows = sample_rows(w.B, w.H, w.Nq, n_rows)
+        say(f"  oracle ({rows.size} sampled rows)")
+        ref = oracle.attention_rows(q, k, v, rows, scale=w.scale, causal=w.causal)
+        err = max_err(o.reshape(-1, w.dv)[rows], ref)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL[w.dtype] * w.sigma_v
+
+
+def test_workload_single_head_f32():
+    _check_workload("single_head_f32_n128_d64", None, "f32")
+
+
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_workload_mha_d64(out_dtype):
+    _check_workload("mha_b4h8_n1024_d64_bf16", None, out_dtype)
+
+
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_workload_causal_4k(out_dtype):
+    _check_workload("causal_b2h16_n4096_d128_bf16", 384, out_dtype)
+
+
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_workload_causal_16k_wide_logits(out_dtype):
+    _check_workload("causal_long_b1h32_n16384_d128_bf16_qk_sigma3", 192, out_dtype)
+
+
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_workload_decode(out_dtype):
+    _check_workload("decode_b64h32_nk8192_d128_bf16", 512, out_dtype)
