@@ -15,7 +15,7 @@ MI355X peaks.  The fp64 CPU oracle is timed on a bounded sample of the
 prefill workload on the host's cores as a reported baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline] [--no-decode]
+                       [--no-cpu-baseline] [--no-decode] [--calibrate-copy MIB]
 """
 from __future__ import annotations
 
@@ -121,6 +121,9 @@ def main(argv=None):
     ap.add_argument("--decode-workload", default=DEFAULT_DECODE)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="before timing, run one plain copy kernel of MIB MiB (read MIB, "
+                         "write MIB) so profiler byte counters can be scaled against it")
     ap.add_argument("--out-dtype", choices=["bf16", "f32"], default=None,
                     help="output storage (default: the input storage type)")
     args = ap.parse_args(argv)
@@ -139,6 +142,15 @@ def main(argv=None):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)          # elementwise: reads n*4 bytes, writes n*4 bytes
+        torch.cuda.synchronize()
+        del src, dst
 
     def run_workload(name):
         w = synth.WORKLOADS[name]

@@ -81,6 +81,28 @@ inline hipError_t launch_kernel(void (*kernel)(Params...), dim3 grid, dim3 block
     return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, 0, stream);
 }
 
+// Raw buffer access: a descriptor over [base, base + bytes).  Loads beyond
+// `bytes` return zeros instead of touching memory, which is how ragged tiles
+// are padded without per-lane clamping.  (Descriptor word 3 for gfx9-family.)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voffset) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voffset, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Combine the two half-waves (lanes l and l ^ 32) with v_permlane32_swap:
+// swapping x with itself leaves {x[l % 32], x[l % 32 + 32]} in every lane.
+__device__ __forceinline__ float half_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Wave-uniform "any lane" test.
 __device__ __forceinline__ bool wave_any(bool pred) { return __ballot(pred) != 0; }
 

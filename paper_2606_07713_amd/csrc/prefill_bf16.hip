@@ -24,6 +24,8 @@
 // 2^kRescaleSlack are accumulated against the stale maximum.  The final
 // O = acc / l uses the same maximum for numerator and denominator, so the
 // result is the same softmax (Steps I-IV regrouped over key tiles).
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
     void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
     using T = Tile<D>;
+    constexpr uint32_t ROW_BYTES = D * 2;
     __shared__ __attribute__((aligned(16))) u16 Ks[T::K_ELEMS];
     __shared__ __attribute__((aligned(16))) u16 Vt[T::V_ELEMS];
 
@@ -92,14 +95,17 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
     c = fabsf(c);
 
     // ---- a1: Q fragment for this lane's query, all of d, kept in registers.
+    // Rows past Nq read as zeros (buffer bounds) and are never stored.
     const int qrow = q0 + wave * 32 + col;
-    const int qrow_c = qrow < Nq ? qrow : Nq - 1;
     bf16x8 qf[D / 16];
+    {
+        const auto rq = make_rsrc(Qh, (uint32_t)Nq * ROW_BYTES);
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-        uint4 w = *reinterpret_cast<const uint4*>(Qh + (size_t)qrow_c * D + s * 16 + half * 8);
-        w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
-        qf[s] = __builtin_bit_cast(bf16x8, w);
+        for (int s = 0; s < D / 16; ++s) {
+            uint4 w = buffer_load16(rq, (uint32_t)qrow * ROW_BYTES + s * 32 + half * 16);
+            w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
+            qf[s] = __builtin_bit_cast(bf16x8, w);
+        }
     }
 
     // Key range this tile of queries needs.
@@ -110,27 +116,28 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
     const int wave_q_last = wave_q_first + 31;
 
     // ---- a2: register staging of one K/V tile (global -> regs -> LDS).
+    // Per-thread byte offsets inside a tile are fixed; each tile only moves the
+    // buffer base, and keys past Nk read as zeros.
     uint4 kreg[T::K_PASSES];
-    uint4 vreg[4];
+    uint4 vreg0, vreg1, vreg2, vreg3;
     const bool v_loader = tid < T::V_THREADS;
     const int v_kg = tid % (BN / 4);      // keys 4*v_kg .. 4*v_kg+3
     const int v_dg = tid / (BN / 4);      // dv 8*v_dg .. 8*v_dg+7
+    const uint32_t v_off = (uint32_t)(4 * v_kg) * ROW_BYTES + v_dg * 16;
 
     auto load_tile = [&](int kt) {
         const int kbase = kt * BN;
+        const uint32_t bytes = (uint32_t)(Nk - kbase) * ROW_BYTES;
+        const auto rk = make_rsrc(Kh + (size_t)kbase * D, bytes);
 #pragma unroll
-        for (int p = 0; p < T::K_PASSES; ++p) {
-            const int idx = tid + p * THREADS;
-            const int row = idx / (D / 8), ch = idx % (D / 8);
-            const int key = min(kbase + row, Nk - 1);
-            kreg[p] = *reinterpret_cast<const uint4*>(Kh + (size_t)key * D + ch * 8);
-        }
+        for (int p = 0; p < T::K_PASSES; ++p)
+            kreg[p] = buffer_load16(rk, (uint32_t)(tid + p * THREADS) * 16);
         if (v_loader) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = min(kbase + 4 * v_kg + r, Nk - 1);
-                vreg[r] = *reinterpret_cast<const uint4*>(Vh + (size_t)key * D + v_dg * 8);
-            }
+            const auto rv = make_rsrc(Vh + (size_t)kbase * D, bytes);
+            vreg0 = buffer_load16(rv, v_off);
+            vreg1 = buffer_load16(rv, v_off + ROW_BYTES);
+            vreg2 = buffer_load16(rv, v_off + 2 * ROW_BYTES);
+            vreg3 = buffer_load16(rv, v_off + 3 * ROW_BYTES);
         }
     };
     auto store_tile = [&]() {
@@ -142,21 +149,26 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
         }
         if (v_loader) {
             // transpose 4 keys x 8 dv into V^T rows: element (dv, key)
-            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                uint2 lo, hi;   // dv = 8*v_dg + 2e (lo halves) and + 2e + 1 (hi halves)
-                lo.x = (w0[e] & 0xffffu) | (w1[e] << 16);
-                lo.y = (w2[e] & 0xffffu) | (w3[e] << 16);
-                hi.x = (w0[e] >> 16) | (w1[e] & 0xffff0000u);
-                hi.y = (w2[e] >> 16) | (w3[e] & 0xffff0000u);
-                const int dv = v_dg * 8 + 2 * e;
-                *reinterpret_cast<uint2*>(&Vt[dv * T::VSTRIDE + 4 * v_kg]) = lo;
-                *reinterpret_cast<uint2*>(&Vt[(dv + 1) * T::VSTRIDE + 4 * v_kg]) = hi;
-            }
+            u16* dst = &Vt[(v_dg * 8) * T::VSTRIDE + 4 * v_kg];
+            auto put = [&](int j, uint32_t a, uint32_t b, uint32_t cc, uint32_t d, bool hi) {
+                uint2 w;
+                if (!hi) {
+                    w.x = __builtin_amdgcn_perm(b, a, 0x05040100u);
+                    w.y = __builtin_amdgcn_perm(d, cc, 0x05040100u);
+                } else {
+                    w.x = __builtin_amdgcn_perm(b, a, 0x07060302u);
+                    w.y = __builtin_amdgcn_perm(d, cc, 0x07060302u);
+                }
+                *reinterpret_cast<uint2*>(dst + j * T::VSTRIDE) = w;
+            };
+            put(0, vreg0.x, vreg1.x, vreg2.x, vreg3.x, false);
+            put(1, vreg0.x, vreg1.x, vreg2.x, vreg3.x, true);
+            put(2, vreg0.y, vreg1.y, vreg2.y, vreg3.y, false);
+            put(3, vreg0.y, vreg1.y, vreg2.y, vreg3.y, true);
+            put(4, vreg0.z, vreg1.z, vreg2.z, vreg3.z, false);
+            put(5, vreg0.z, vreg1.z, vreg2.z, vreg3.z, true);
+            put(6, vreg0.w, vreg1.w, vreg2.w, vreg3.w, false);
+            put(7, vreg0.w, vreg1.w, vreg2.w, vreg3.w, true);
         }
     };
 
@@ -166,15 +178,10 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
     float m_run = kNegInf;   // running max, log2 units (scores * c)
     float l_run = 0.0f;      // partial denominator over this half-wave's keys
 
-    load_tile(0);
-    for (int kt = 0; kt < n_kt; ++kt) {
-        __syncthreads();            // previous tile fully consumed
-        store_tile();
-        __syncthreads();            // tile visible to all waves
-        if (kt + 1 < n_kt) load_tile(kt + 1);
-
-        const int kbase = kt * BN;
-        if (CAUSAL && kbase > wave_q_last + off) continue;   // tile fully masked for this wave
+    // One key tile for this wave: a3..a6.  MASK selects the variant for tiles
+    // that contain keys past Nk or past some query's diagonal.
+    auto compute_tile = [&](const int kbase, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
 
         // ---- a3: S^T tile (64 keys x 32 queries) = K_tile . Q^T on MFMA.
         f32x16 sacc[BN / 32];
@@ -189,10 +196,7 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[kb], 0, 0, 0);
             }
         }
-
-        // Mask keys past Nk and (causal) keys after the query's diagonal.
-        const bool need_mask = (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
-        if (need_mask) {
+        if constexpr (MASK) {
 #pragma unroll
             for (int kb = 0; kb < BN / 32; ++kb) {
 #pragma unroll
@@ -210,8 +214,8 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
         for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mt = (mx == kNegInf) ? kNegInf : mx * c;
+        mx = half_max(mx);
+        const float mt = (MASK && mx == kNegInf) ? kNegInf : mx * c;
 
         // Raise the reference maximum only when the tile exceeds it by the slack.
         if (wave_any(mt > m_run + kRescaleSlack)) {
@@ -231,7 +235,7 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 float p = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
-                if (need_mask && sacc[kb][i] == kNegInf) p = 0.0f;
+                if constexpr (MASK) p = (sacc[kb][i] == kNegInf) ? 0.0f : p;
                 l_run += p;
                 pb[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
             }
@@ -251,10 +255,26 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
                     __builtin_bit_cast(bf16x8, w), pb[cc], oacc[b], 0, 0, 0);
             }
         }
+    };
+
+    load_tile(0);
+    for (int kt = 0; kt < n_kt; ++kt) {
+        __syncthreads();            // previous tile fully consumed
+        store_tile();
+        __syncthreads();            // tile visible to all waves
+        if (kt + 1 < n_kt) load_tile(kt + 1);
+
+        const int kbase = kt * BN;
+        if (CAUSAL && kbase > wave_q_last + off) continue;   // tile fully masked for this wave
+        const bool need_mask = (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
+        if (need_mask)
+            compute_tile(kbase, std::true_type{});
+        else
+            compute_tile(kbase, std::false_type{});
     }
 
     // ---- a7: epilogue, O = acc / l: the only device-memory write.
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
     if (qrow < Nq) {
         const size_t obase = ((size_t)bh * Nq + qrow) * D;
