@@ -108,7 +108,11 @@ int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk
  * Computation: inner products and softmax statistics in fp32 from exact
  * products of the inputs; bf16 inputs use bf16 matrix-core products with fp32
  * accumulation and the unnormalised weights rounded to bf16 before they
- * multiply V.  Results are deterministic: identical inputs give bit-identical
+ * multiply V.  For bf16 prefill the denominator is the sum of those same
+ * rounded weights, so O is an exact convex combination of V rows with weights
+ * within 2^-8 (relative) of the softmax, and LSE is within ln(1 + 2^-8) of the
+ * exact value; fp32 inputs and decode-shaped calls keep fp32 weights
+ * throughout.  Results are deterministic: identical inputs give bit-identical
  * outputs (no atomics).
  *
  * Returns MOA_OK once the work is enqueued (or when B*H*Nq == 0: nothing is

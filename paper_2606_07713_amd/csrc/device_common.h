@@ -92,6 +92,21 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 16 bytes per lane from a buffer straight into LDS (buffer_load_dwordx4 ...
+// lds): lane l's data lands at lds_base + 16*l, lds_base being wave-uniform.
+// The builtin exists only for the device pass; in the host pass a call to it
+// makes clang drop the kernel's host-side stub, so the host pass sees an empty
+// body (it never runs device code).
+__device__ __forceinline__ void buffer_load16_to_lds(__amdgpu_buffer_rsrc_t r, void* lds_base,
+                                                     uint32_t voffset) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        r, (__attribute__((address_space(3))) void*)lds_base, 16, voffset, 0, 0, 0);
+#else
+    (void)r; (void)lds_base; (void)voffset;
+#endif
+}
+
 // Combine the two half-waves (lanes l and l ^ 32) with v_permlane32_swap:
 // swapping x with itself leaves {x[l % 32], x[l % 32 + 32]} in every lane.
 __device__ __forceinline__ float half_max(float x) {

@@ -35,7 +35,7 @@ hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream);
 hipError_t launch_decode(const Problem& p, int splits, float* ws, hipStream_t stream);
 
 // Row-tile size of the bf16 prefill kernel (queries per workgroup).
-constexpr int kPrefillBf16RowsPerBlock = 128;
+constexpr int kPrefillBf16RowsPerBlock = 256;
 // Row-tile size of the fp32 prefill kernel.
 constexpr int kPrefillF32RowsPerBlock = 64;
 

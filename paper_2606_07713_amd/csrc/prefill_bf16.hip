@@ -1,29 +1,43 @@
 // Fused attention prefill for bf16 inputs on gfx950 matrix cores.
 //
-// One workgroup owns one (batch*head, 128-query tile).  It keeps its Q tile in
-// registers for the whole key loop, streams K and V through LDS one 64-key
-// tile at a time, and never writes anything but the output (and optional LSE)
-// to device memory: the score tile, the exponentials and the running softmax
-// statistics live in registers only (the DNF of eqs. dnf_attn / output_dnf).
+// One workgroup owns one (batch*head, 256-query tile) and runs 8 waves of 32
+// queries each.  The Q tile stays in registers for the whole key loop, K and V
+// stream through LDS in 64-key tiles, and nothing but the output (and the
+// optional LSE) is ever written to device memory: scores, exponentials and the
+// running softmax statistics live in registers only (the DNF of eqs. dnf_attn
+// and output_dnf: no K^T buffer, no score matrix, no softmax temporary).
 //
 // Orientation.  Each wave computes the transposed score tile S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16: K rows are the A operand read straight from LDS in
-// their stored order, so no K^T is ever formed (eq. mm_psi reads K by row).
-// In the accumulator layout every lane then holds scores of ONE query
-// (column = lane % 32) for 16 of the tile's keys, and lane l ^ 32 holds the
-// other keys of the same query, so the row max (Step I) and row sum (Step III)
-// are in-lane reductions plus one exchange between the two half-waves.
-// The output is accumulated transposed too, O^T += V^T P^T: the P^T operand
-// is the score accumulator re-packed to bf16 in place (no data movement), and
-// V^T comes from an LDS copy of the V tile stored dv-major.
+// v_mfma_f32_32x32x16_bf16: K rows are the A operand, read in their stored
+// order, so no K^T is ever formed (eq. mm_psi reads K by row).  In the
+// accumulator layout a lane holds scores of ONE query (column = lane % 32) for
+// 16 keys and lane l ^ 32 holds the other 16 keys of the same query, so the
+// row max (Step I) and row sum (Step III) are in-lane reductions plus one
+// v_permlane32_swap.  The output is accumulated transposed as well,
+// O^T += V^T P^T: the P^T operand is the score accumulator converted to bf16
+// in place, and the V^T operand is read from the row-major V tile with
+// ds_read_b64_tr_b16 (a transposing LDS read), so V is never transposed either.
+//
+// Data movement.  K and V tiles go from device memory straight into LDS
+// (buffer_load ... lds, 16 bytes per lane, no register staging) through
+// two-stage rings; rows past Nk come back as zeros from the buffer bounds.
+// LDS rows are stored with a 16-byte-chunk XOR swizzle instead of padding,
+// because direct-to-LDS writes are contiguous per instruction.
+//
+// Ping-pong.  Waves w and w + 4 share a SIMD.  The workgroup advances in
+// phases separated by barriers; in each phase one group of four waves issues
+// the matrix products of a tile (P(t-1) V(t-1) and S(t) = K(t) Q^T) while the
+// other group runs the softmax of its previous tile on the vector ALU, and the
+// groups swap roles every phase.  This keeps the matrix cores and the vector
+// ALU of every SIMD busy at the same time.
 //
 // Softmax.  Scores are kept in raw units; with c = scale * log2(e) the weight
 // of key j is 2^(s_j c - m) where m is a running row maximum in log2 units.
-// The running maximum is only raised (and O, l rescaled) when the tile max
-// exceeds it by more than kRescaleSlack; otherwise weights up to
-// 2^kRescaleSlack are accumulated against the stale maximum.  The final
-// O = acc / l uses the same maximum for numerator and denominator, so the
-// result is the same softmax (Steps I-IV regrouped over key tiles).
+// The reference maximum is raised (and O, l rescaled) only when a tile exceeds
+// it by more than kRescaleSlack; otherwise weights up to 2^kRescaleSlack are
+// accumulated against the stale maximum.  The final O = acc / l uses the same
+// reference for numerator and denominator, so the result is the same softmax
+// (Steps I-IV regrouped over key tiles).
 #include <type_traits>
 
 #include "device_common.h"
@@ -32,24 +46,44 @@
 namespace moa {
 namespace {
 
-constexpr int BM = 128;          // queries per workgroup
-constexpr int BN = 64;           // keys per tile
-constexpr int WAVES = 4;         // each wave: 32 queries
+constexpr int WAVES = 8;         // two groups of four; wave w and w + 4 share a SIMD
 constexpr int THREADS = WAVES * 64;
+constexpr int BM = WAVES * 32;   // queries per workgroup
+constexpr int BN = 64;           // keys per tile
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kFastSumLimit = 1048576.0f;   // 2^20
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 template <int D>
-struct Tile {
-    static constexpr int KSTRIDE = D + 8;    // K tile row stride (elements): rows shift 4 banks
-    static constexpr int VSTRIDE = BN + 4;   // V^T row stride (elements)
-    static constexpr int K_ELEMS = BN * KSTRIDE;
-    static constexpr int V_ELEMS = D * VSTRIDE;
-    static constexpr int K_CHUNKS = BN * D / 8;             // 16-byte chunks per K tile
-    static constexpr int K_PASSES = K_CHUNKS / THREADS;     // 16-byte loads per thread
-    static constexpr int V_THREADS = (D / 8) * (BN / 4);    // threads loading 4 keys x 8 dv
-    static_assert(K_CHUNKS % THREADS == 0, "K tile must split evenly");
-    static_assert(V_THREADS <= THREADS, "V tile too large");
+struct Cfg {
+    static constexpr int CHUNKS = D / 8;                        // 16-byte chunks per row
+    static constexpr uint32_t ROW_BYTES = D * 2;
+    static constexpr uint32_t TILE_BYTES = BN * ROW_BYTES;      // one K or V tile
+    static constexpr int LOADS_PER_WAVE = TILE_BYTES / (WAVES * 1024);
+    static_assert(TILE_BYTES % (WAVES * 1024) == 0, "tile must split into wave loads");
 };
+
+// 16-byte-chunk XOR swizzle of LDS row `row` (a permutation of the row's
+// chunks).  With 64 four-byte banks: the K operand reads (16 lanes, 16
+// consecutive rows, one logical chunk) hit 16 distinct bank groups, and the
+// transposing V reads (32 lanes: 4 rows x 2 chunks x 2 halves per 16 lanes)
+// hit 64 distinct banks -- for d = 128 together with the dv order below.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+    if constexpr (D == 128) return ((row & 3) << 1) | (((row >> 2) & 1) << 3) | ((row >> 3) & 1);
+    return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+}
+
+// dv index held by row m (0..31) of the b-th O^T accumulator block.  For d =
+// 128 the two 16-row halves of a block take dv ranges 64 apart, so the two
+// 16-lane groups of a transposing read touch opposite bank halves.
+template <int D>
+__device__ __forceinline__ int dv_of(int b, int m) {
+    if constexpr (D == 128) return (m < 16) ? 16 * b + m : 64 + 16 * b + (m - 16);
+    return 32 * b + m;
+}
 
 // Workgroup index -> (head slice, query tile), keeping the query tiles of one
 // head on one XCD (workgroups are handed to the 8 XCDs round-robin) so that
@@ -65,18 +99,36 @@ __device__ __forceinline__ void tile_of_block(int bid, int nblocks, int n_qtiles
     qt = causal ? (n_qtiles - 1 - t) : t;
 }
 
+__device__ __forceinline__ void wait_loads_to_lds() {
+    __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's LDS-bound loads have landed
+}
+
 template <int D, bool CAUSAL, bool OUT_BF16>
-__global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
+__global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
     void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
-    using T = Tile<D>;
-    constexpr uint32_t ROW_BYTES = D * 2;
-    __shared__ __attribute__((aligned(16))) u16 Ks[T::K_ELEMS];
-    __shared__ __attribute__((aligned(16))) u16 Vt[T::V_ELEMS];
+    using C = Cfg<D>;
+    constexpr uint32_t RB = C::ROW_BYTES;
+    // One LDS array per ring stage: the compiler tracks direct-to-LDS loads per
+    // underlying object, so reads of one stage need not wait for loads still
+    // landing in another.
+    __shared__ __attribute__((aligned(1024))) unsigned char k_st0[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char k_st1[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_st0[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_st1[C::TILE_BYTES];
+    auto k_stage = [&](auto tag) -> unsigned char* {
+        if constexpr (decltype(tag)::value == 0) return k_st0; else return k_st1;
+    };
+    auto v_stage = [&](auto tag) -> unsigned char* {
+        if constexpr (decltype(tag)::value == 0) return v_st0; else return v_st1;
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    const int grp = wave >> 2;     // 0: leads by one phase, 1: trails
     const int col = lane & 31;     // query within the wave's 32
     const int half = lane >> 5;    // which 8-element k group of the MFMA operands
 
@@ -99,116 +151,149 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
     const int qrow = q0 + wave * 32 + col;
     bf16x8 qf[D / 16];
     {
-        const auto rq = make_rsrc(Qh, (uint32_t)Nq * ROW_BYTES);
+        const auto rq = make_rsrc(Qh, (uint32_t)Nq * RB);
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) {
-            uint4 w = buffer_load16(rq, (uint32_t)qrow * ROW_BYTES + s * 32 + half * 16);
+            uint4 w = buffer_load16(rq, (uint32_t)qrow * RB + s * 32 + half * 16);
             w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
             qf[s] = __builtin_bit_cast(bf16x8, w);
         }
     }
 
-    // Key range this tile of queries needs.
+    // Key tiles this workgroup needs, and those this wave needs.
     int kv_end = Nk;
     if (CAUSAL) kv_end = min(Nk, q0 + BM + off);
     const int n_kt = (kv_end + BN - 1) / BN;
     const int wave_q_first = q0 + wave * 32;
-    const int wave_q_last = wave_q_first + 31;
+    int n_w = n_kt;
+    if (CAUSAL) n_w = min(n_kt, (wave_q_first + 31 + off) / BN + 1);
 
-    // ---- a2: register staging of one K/V tile (global -> regs -> LDS).
-    // Per-thread byte offsets inside a tile are fixed; each tile only moves the
-    // buffer base, and keys past Nk read as zeros.
-    uint4 kreg[T::K_PASSES];
-    uint4 vreg0, vreg1, vreg2, vreg3;
-    const bool v_loader = tid < T::V_THREADS;
-    const int v_kg = tid % (BN / 4);      // keys 4*v_kg .. 4*v_kg+3
-    const int v_dg = tid / (BN / 4);      // dv 8*v_dg .. 8*v_dg+7
-    const uint32_t v_off = (uint32_t)(4 * v_kg) * ROW_BYTES + v_dg * 16;
+    // ---- a2: direct-to-LDS tile loads.  Lane l of the wave's i-th load fills
+    // LDS slot S = (wave*L + i)*64 + l, which holds logical chunk
+    // (S % CHUNKS) ^ swz(row) of row S / CHUNKS.
+    uint32_t ld_voff[C::LOADS_PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < C::LOADS_PER_WAVE; ++i) {
+        const int slot = (wave * C::LOADS_PER_WAVE + i) * 64 + lane;
+        const int row = slot / C::CHUNKS, p = slot % C::CHUNKS;
+        ld_voff[i] = (uint32_t)row * RB + (uint32_t)((p ^ swz<D>(row)) * 16);
+    }
+    auto issue_tile_load = [&](const u16* head, int kbase, unsigned char* stage) {
+        const auto r = make_rsrc(head + (size_t)kbase * D, (uint32_t)(Nk - kbase) * RB);
+#pragma unroll
+        for (int i = 0; i < C::LOADS_PER_WAVE; ++i)
+            buffer_load16_to_lds(r, stage + (wave * C::LOADS_PER_WAVE + i) * 1024, ld_voff[i]);
+    };
 
-    auto load_tile = [&](int kt) {
-        const int kbase = kt * BN;
-        const uint32_t bytes = (uint32_t)(Nk - kbase) * ROW_BYTES;
-        const auto rk = make_rsrc(Kh + (size_t)kbase * D, bytes);
+    // Per-lane LDS addresses of the MFMA operand reads (stage, key block and
+    // key chunk are added as immediates).
+    uint32_t kaddr[D / 16];          // K rows: row = col (+32 kb), chunk 2s + half
 #pragma unroll
-        for (int p = 0; p < T::K_PASSES; ++p)
-            kreg[p] = buffer_load16(rk, (uint32_t)(tid + p * THREADS) * 16);
-        if (v_loader) {
-            const auto rv = make_rsrc(Vh + (size_t)kbase * D, bytes);
-            vreg0 = buffer_load16(rv, v_off);
-            vreg1 = buffer_load16(rv, v_off + ROW_BYTES);
-            vreg2 = buffer_load16(rv, v_off + 2 * ROW_BYTES);
-            vreg3 = buffer_load16(rv, v_off + 3 * ROW_BYTES);
-        }
-    };
-    auto store_tile = [&]() {
+    for (int s = 0; s < D / 16; ++s)
+        kaddr[s] = (uint32_t)col * RB + (uint32_t)(((2 * s + half) ^ swz<D>(col)) * 16);
+    uint32_t vaddr[D / 32][2];       // V rows for ds_read_b64_tr_b16 (lo / hi key quads)
+    {
+        const int g = lane >> 4, j = (lane >> 2) & 3, q = lane & 3;
 #pragma unroll
-        for (int p = 0; p < T::K_PASSES; ++p) {
-            const int idx = tid + p * THREADS;
-            const int row = idx / (D / 8), ch = idx % (D / 8);
-            *reinterpret_cast<uint4*>(&Ks[row * T::KSTRIDE + ch * 8]) = kreg[p];
-        }
-        if (v_loader) {
-            // transpose 4 keys x 8 dv into V^T rows: element (dv, key)
-            u16* dst = &Vt[(v_dg * 8) * T::VSTRIDE + 4 * v_kg];
-            auto put = [&](int j, uint32_t a, uint32_t b, uint32_t cc, uint32_t d, bool hi) {
-                uint2 w;
-                if (!hi) {
-                    w.x = __builtin_amdgcn_perm(b, a, 0x05040100u);
-                    w.y = __builtin_amdgcn_perm(d, cc, 0x05040100u);
-                } else {
-                    w.x = __builtin_amdgcn_perm(b, a, 0x07060302u);
-                    w.y = __builtin_amdgcn_perm(d, cc, 0x07060302u);
-                }
-                *reinterpret_cast<uint2*>(dst + j * T::VSTRIDE) = w;
-            };
-            put(0, vreg0.x, vreg1.x, vreg2.x, vreg3.x, false);
-            put(1, vreg0.x, vreg1.x, vreg2.x, vreg3.x, true);
-            put(2, vreg0.y, vreg1.y, vreg2.y, vreg3.y, false);
-            put(3, vreg0.y, vreg1.y, vreg2.y, vreg3.y, true);
-            put(4, vreg0.z, vreg1.z, vreg2.z, vreg3.z, false);
-            put(5, vreg0.z, vreg1.z, vreg2.z, vreg3.z, true);
-            put(6, vreg0.w, vreg1.w, vreg2.w, vreg3.w, false);
-            put(7, vreg0.w, vreg1.w, vreg2.w, vreg3.w, true);
-        }
-    };
+        for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+            for (int h8 = 0; h8 < 2; ++h8) {
+                const int row = 4 * (g >> 1) + j + 8 * h8;
+                const int dv = dv_of<D>(b, 16 * (g & 1) + 4 * q);
+                vaddr[b][h8] = (uint32_t)row * RB + (uint32_t)((((dv >> 3) ^ swz<D>(row)) * 16) +
+                                                               (dv & 7) * 2);
+            }
+    }
 
     f32x16 oacc[D / 32];
 #pragma unroll
     for (int b = 0; b < D / 32; ++b) oacc[b] = f32x16{};
-    float m_run = kNegInf;   // running max, log2 units (scores * c)
-    float l_run = 0.0f;      // partial denominator over this half-wave's keys
+    f32x16 sacc[BN / 32];            // S^T of the current tile
+    bf16x8 pbuf[BN / 16];            // bf16 P^T of the current tile
+    float m_run = kNegInf;           // running reference max, log2 units (scores * c)
+    float l_run = 0.0f;              // partial denominator over this half-wave's keys
+    float alpha_pend = 1.0f;         // rescale owed to oacc before the next P.V
+    bool rescale_pend = false;
 
-    // One key tile for this wave: a3..a6.  MASK selects the variant for tiles
-    // that contain keys past Nk or past some query's diagonal.
-    auto compute_tile = [&](const int kbase, auto mask_tag) {
-        constexpr bool MASK = decltype(mask_tag)::value;
-
-        // ---- a3: S^T tile (64 keys x 32 queries) = K_tile . Q^T on MFMA.
-        f32x16 sacc[BN / 32];
+    // ---- a3: S^T(t) = K_t . Q^T from K stage B.
+    auto s_mfma = [&](auto stage_tag) {
+        const unsigned char* ks = k_stage(stage_tag);
 #pragma unroll
         for (int kb = 0; kb < BN / 32; ++kb) sacc[kb] = f32x16{};
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
+        for (int s = 0; s < D / 16; ++s)
 #pragma unroll
             for (int kb = 0; kb < BN / 32; ++kb) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    &Ks[(kb * 32 + col) * T::KSTRIDE + s * 16 + half * 8]);
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + kaddr[s] + kb * 32 * RB);
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[kb], 0, 0, 0);
             }
-        }
-        if constexpr (MASK) {
+    };
+
+    // ---- a6: O^T += V^T . P^T from V stage B.  Chunk cc covers keys
+    // 16cc + 4*half + {0..3} and 16cc + 8 + 4*half + {0..3}, which is both the
+    // key order of pbuf (the S^T accumulator layout) and that of the two
+    // transposing reads.
+    auto pv_mfma = [&](auto stage_tag) {
+        unsigned char* vs = v_stage(stage_tag);
 #pragma unroll
-            for (int kb = 0; kb < BN / 32; ++kb) {
+        for (int cc = 0; cc < BN / 16; ++cc)
+#pragma unroll
+            for (int b = 0; b < D / 32; ++b) {
+                const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4s*)(vs + vaddr[b][0] + cc * 16 * RB));
+                const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4s*)(vs + vaddr[b][1] + cc * 16 * RB));
+                const v4s both[2] = {lo, hi};
+                oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, both), pbuf[cc], oacc[b], 0, 0, 0);
+            }
+    };
+
+    // ---- a4 + a5: softmax of tile t from sacc into pbuf.
+    //
+    // Weights are p = 2^(s c - m) against the running reference m, rounded to
+    // bf16 for the P.V product; the denominator sums exactly those rounded
+    // weights (v_dot2_f32_bf16 against ones), so numerator and denominator use
+    // the same p.  exp_pack() returns the tile's partial sum.
+    auto exp_pack = [&](float neg_m, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+        float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) {
+                float p0 = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
+                float p1 = exp2_hw(__builtin_fmaf(sacc[kb][i + 1], c, neg_m));
+                if constexpr (MASK) {
+                    p0 = (sacc[kb][i] == kNegInf) ? 0.0f : p0;
+                    p1 = (sacc[kb][i + 1] == kNegInf) ? 0.0f : p1;
+                }
+                const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
+                pbuf[kb * 2 + (i >> 3)][i & 7] = pp[0];
+                pbuf[kb * 2 + (i >> 3)][(i & 7) + 1] = pp[1];
+                part[(i >> 1) & 3] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, part[(i >> 1) & 3], false);
+            }
+        return (part[0] + part[1]) + (part[2] + part[3]);
+    };
+
+    // Full step: tile max (Step I), raise the reference when it outgrew the
+    // slack, then the weights.  Used for masked tiles and whenever the fast
+    // step's check fails.
+    auto softmax_full = [&](int t, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        if constexpr (MASK) {
+            const int kbase = t * BN;
+#pragma unroll
+            for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int key = kbase + kb * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
                     const bool masked = key >= Nk || (CAUSAL && key > qrow + off);
                     if (masked) sacc[kb][i] = kNegInf;
                 }
-            }
         }
-
-        // ---- a4: tile row max (in-lane, then across the two half-waves).
         float mx = kNegInf;
 #pragma unroll
         for (int kb = 0; kb < BN / 32; ++kb)
@@ -216,61 +301,81 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
         mx = half_max(mx);
         const float mt = (MASK && mx == kNegInf) ? kNegInf : mx * c;
-
-        // Raise the reference maximum only when the tile exceeds it by the slack.
-        if (wave_any(mt > m_run + kRescaleSlack)) {
+        const bool need = wave_any(mt > m_run + kRescaleSlack);
+        if (need) {
             const float m_new = fmaxf(m_run, mt);
-            const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
+            const float alpha = exp2_hw(m_run - m_new);
             l_run *= alpha;
-#pragma unroll
-            for (int b = 0; b < D / 32; ++b) oacc[b] *= alpha;
+            alpha_pend = rescale_pend ? alpha_pend * alpha : alpha;
+            rescale_pend = true;
             m_run = m_new;
         }
+        l_run += exp_pack(-m_run, mask_tag);
+    };
 
-        // ---- a5: weights p = 2^(s c - m), partial row sum, pack to bf16.
-        const float neg_m = -m_run;
-        bf16x8 pb[BN / 16];
+    // Fast step for interior tiles: no max.  The weights are taken against
+    // the current reference directly; if any tile's partial sum exceeds
+    // 2^kFastSumLimit (or overflowed), the tile is redone by the full step.
+    // Any reference gives the same quotient, so this is exact; it only skips
+    // Step I's max while the reference is still close enough to it.
+    auto softmax_fast = [&](int t) {
+        const float part = exp_pack(-m_run, std::false_type{});
+        if (wave_any(!(part <= kFastSumLimit))) softmax_full(t, std::false_type{});
+        else l_run += part;
+    };
+    auto tile_needs_mask = [&](int t) {
+        const int kbase = t * BN;
+        return (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
+    };
+
+    // Matrix phase of tile t: P(t-1) V(t-1) then S(t).  K(t) sits in K stage
+    // t & 1 and V(t-1) in V stage (t-1) & 1 = PAR ^ 1.
+    auto gemm_phase = [&](int t, auto par_tag) {
+        constexpr int P = decltype(par_tag)::value;
+        if (rescale_pend) {
 #pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                float p = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
-                if constexpr (MASK) p = (sacc[kb][i] == kNegInf) ? 0.0f : p;
-                l_run += p;
-                pb[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
-            }
+            for (int b = 0; b < D / 32; ++b) oacc[b] *= alpha_pend;
+            rescale_pend = false;
         }
-
-        // ---- a6: O^T += V^T . P^T on MFMA.  Chunk cc covers keys
-        // 16cc + 4*half + {0..3} and 16cc + 8 + 4*half + {0..3}, matching pb.
-#pragma unroll
-        for (int cc = 0; cc < BN / 16; ++cc) {
-#pragma unroll
-            for (int b = 0; b < D / 32; ++b) {
-                const u16* vrow = &Vt[(b * 32 + col) * T::VSTRIDE + cc * 16 + half * 4];
-                const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-                const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-                const uint4 w = make_uint4(lo.x, lo.y, hi.x, hi.y);
-                oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, w), pb[cc], oacc[b], 0, 0, 0);
-            }
+        if (t >= 1 && t - 1 < n_w) pv_mfma(std::integral_constant<int, 1 - P>{});
+        if (t < n_w) s_mfma(std::integral_constant<int, P>{});
+    };
+    auto softmax_phase = [&](int t) {
+        if (t < n_w) {
+            if (tile_needs_mask(t) || m_run == kNegInf) softmax_full(t, std::true_type{});
+            else softmax_fast(t);
         }
     };
 
-    load_tile(0);
-    for (int kt = 0; kt < n_kt; ++kt) {
-        __syncthreads();            // previous tile fully consumed
-        store_tile();
-        __syncthreads();            // tile visible to all waves
-        if (kt + 1 < n_kt) load_tile(kt + 1);
-
-        const int kbase = kt * BN;
-        if (CAUSAL && kbase > wave_q_last + off) continue;   // tile fully masked for this wave
-        const bool need_mask = (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
-        if (need_mask)
-            compute_tile(kbase, std::true_type{});
-        else
-            compute_tile(kbase, std::false_type{});
+    // Phases u = 0, 1, 2, ...: the leading group runs gemm(t) in phase 2t and
+    // softmax(t) in phase 2t + 1; the trailing group runs gemm(t) in phase
+    // 2t + 1 and softmax(t) in phase 2t + 2.  K(t+1) and V(t) are loaded during
+    // phases 2t and 2t + 1 into the stages freed by phase 2t - 1.
+    issue_tile_load(Kh, 0, k_st0);
+    wait_loads_to_lds();
+    __syncthreads();
+    for (int t = 0; t <= n_kt; t += 2) {
+        // ---- even tile t (parity 0)
+        if (t + 1 < n_kt) issue_tile_load(Kh, (t + 1) * BN, k_st1);
+        if (t < n_kt) issue_tile_load(Vh, t * BN, v_st0);
+        if (grp == 0) gemm_phase(t, std::integral_constant<int, 0>{});
+        else if (t >= 1) softmax_phase(t - 1);
+        __syncthreads();
+        if (grp == 0) softmax_phase(t);
+        else gemm_phase(t, std::integral_constant<int, 0>{});
+        wait_loads_to_lds();
+        __syncthreads();
+        if (t + 1 > n_kt) break;
+        // ---- odd tile t + 1 (parity 1)
+        if (t + 2 < n_kt) issue_tile_load(Kh, (t + 2) * BN, k_st0);
+        if (t + 1 < n_kt) issue_tile_load(Vh, (t + 1) * BN, v_st1);
+        if (grp == 0) gemm_phase(t + 1, std::integral_constant<int, 1>{});
+        else softmax_phase(t);
+        __syncthreads();
+        if (grp == 0) softmax_phase(t + 1);
+        else gemm_phase(t + 1, std::integral_constant<int, 1>{});
+        wait_loads_to_lds();
+        __syncthreads();
     }
 
     // ---- a7: epilogue, O = acc / l: the only device-memory write.
@@ -282,7 +387,7 @@ __global__ __launch_bounds__(THREADS, 2) void prefill_bf16_kernel(
         for (int b = 0; b < D / 32; ++b) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int dv = b * 32 + g * 8 + half * 4;
+                const int dv = dv_of<D>(b, g * 8 + half * 4);
                 const float o0 = oacc[b][g * 4 + 0] * inv, o1 = oacc[b][g * 4 + 1] * inv;
                 const float o2 = oacc[b][g * 4 + 2] * inv, o3 = oacc[b][g * 4 + 3] * inv;
                 if (OUT_BF16) {

@@ -50,7 +50,16 @@ def test_prefill_matches_oracle(shape, causal, dtype, out_dtype):
     err = max_err(o, ref)
     say(f"  max err {err:.3e}")
     assert err <= TOL[dtype]
-    assert max_err(lse, ref_lse) <= (1e-5 if dtype == "f32" else 1e-4) * max(1.0, np.abs(ref_lse).max())
+    assert max_err(lse, ref_lse) <= _lse_tol(dtype, ref_lse)
+
+
+def _lse_tol(dtype, ref_lse):
+    # fp32 path: fp32 rounding of the logits.  bf16 path: the denominator is the
+    # sum of the bf16-rounded weights that also multiply V (relative error at
+    # most 2^-8), so LSE is within ln(1 + 2^-8) < 4e-3 plus fp32 rounding.
+    if dtype == "f32":
+        return 1e-5 * max(1.0, np.abs(ref_lse).max())
+    return 4e-3 + 1e-5 * np.abs(ref_lse).max()
 
 
 DECODE_CASES = [
@@ -77,7 +86,7 @@ def test_decode_matches_oracle(case, dtype, out_dtype, causal):
     err = max_err(o, ref)
     say(f"  max err {err:.3e}")
     assert err <= TOL[dtype]
-    assert max_err(lse, ref_lse) <= (1e-5 if dtype == "f32" else 1e-4) * max(1.0, np.abs(ref_lse).max())
+    assert max_err(lse, ref_lse) <= _lse_tol(dtype, ref_lse)
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.125, 0.3])
