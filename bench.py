@@ -56,6 +56,38 @@ def compulsory_bytes(w, out_bytes: int) -> int:
     return w.B * w.H * ((w.Nq * w.dk + w.Nk * (w.dk + w.dv)) * es + w.Nq * w.dv * out_bytes)
 
 
+KERNEL_SOURCES = {
+    "prefill_bf16": ("prefill_bf16.hip", "device_common.h", "launch.h"),
+    "decode_split": ("decode.hip", "device_common.h", "launch.h"),
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """First 16 hex digits of the sha256 of the kernel's source files."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2606_07713_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter passes (profiles/traffic.txt),
+    or None when they were taken on a different kernel source or workload."""
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    want = kernel_source_hash(kernel)
+    with open(path) as fh:
+        for line in fh:
+            parts = line.split()
+            if len(parts) == 4 and not line.startswith("#") and parts[0] == kernel \
+                    and parts[1] == workload and parts[2] == want:
+                return int(parts[3])
+    return None
+
+
 def _inputs(w, dev):
     import synth
     q, k, v = synth.make_inputs(w)
@@ -173,7 +205,8 @@ def main(argv=None):
     mfma_bound = flops / nbytes > PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
     if mfma_bound:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured_traffic("prefill_bf16", w.name) if w.dtype == "bf16" else None}
     else:
         gbs = nbytes / (ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -211,7 +244,7 @@ def main(argv=None):
             "tflops": round(algorithmic_flops(wd) / (msd * 1e-3) / 1e12, 2),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                         "traffic": None},
+                         "traffic": measured_traffic("decode_split", wd.name)},
         }
         print(f"# decode {wd.name}: {msd:.4f} ms/call, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
 
