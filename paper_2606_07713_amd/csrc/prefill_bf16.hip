@@ -48,7 +48,7 @@ namespace {
 
 constexpr int WAVES = 8;         // two groups of four; wave w and w + 4 share a SIMD
 constexpr int THREADS = WAVES * 64;
-constexpr int BM = WAVES * 32;   // queries per workgroup
+constexpr int BM = WAVES * 32;   // queries per workgroup (ping-pong layout)
 constexpr int BN = 64;           // keys per tile
 constexpr float kRescaleSlack = 8.0f;
 constexpr float kFastSumLimit = 1048576.0f;   // 2^20
@@ -103,19 +103,32 @@ __device__ __forceinline__ void wait_loads_to_lds() {
     __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's LDS-bound loads have landed
 }
 
-template <int D, bool CAUSAL, bool OUT_BF16>
+// KSPLIT = false: ping-pong over one key range, 8 waves x 32 queries = 256
+//   queries per workgroup.
+// KSPLIT = true: 4 query blocks x 2 key halves = 128 queries per workgroup;
+//   group g streams key tiles of its half through its own LDS rings (both
+//   groups in the same phase), and group 1 hands its softmax state (m, l, O)
+//   to group 0 through LDS at the end for an exact merge.  Used when the
+//   ping-pong grid is too small to fill the GPU.
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT>
 __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
     void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
-    // One LDS array per ring stage: the compiler tracks direct-to-LDS loads per
-    // underlying object, so reads of one stage need not wait for loads still
-    // landing in another.
-    __shared__ __attribute__((aligned(1024))) unsigned char k_st0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char k_st1[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char v_st0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char v_st1[C::TILE_BYTES];
+    constexpr int NG = KSPLIT ? 2 : 1;                    // independent key streams
+    constexpr int QB = KSPLIT ? WAVES / 2 : WAVES;        // query blocks of 32
+    constexpr int BMQ = QB * 32;                          // queries per workgroup
+    constexpr int LOADERS = WAVES / NG;                   // waves loading one stream
+    constexpr int LPW = C::TILE_BYTES / (LOADERS * 1024); // 16-byte loads per lane per tile
+    static_assert(C::TILE_BYTES % (LOADERS * 1024) == 0, "tile must split into wave loads");
+    // One LDS array per ring stage (each holding one tile per stream): the
+    // compiler tracks direct-to-LDS loads per underlying object, so reads of
+    // one stage need not wait for loads still landing in another.
+    __shared__ __attribute__((aligned(1024))) unsigned char k_st0[NG * C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char k_st1[NG * C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_st0[NG * C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_st1[NG * C::TILE_BYTES];
     auto k_stage = [&](auto tag) -> unsigned char* {
         if constexpr (decltype(tag)::value == 0) return k_st0; else return k_st1;
     };
@@ -128,13 +141,16 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int grp = wave >> 2;     // 0: leads by one phase, 1: trails
+    const int grp = wave >> 2;                       // ping-pong: phase group; key split: key half
+    const int qw = KSPLIT ? (wave & 3) : wave;       // query block of this wave
+    const int lw = KSPLIT ? (wave & 3) : wave;       // index among the waves loading its stream
+    const uint32_t g_off = KSPLIT ? (uint32_t)grp * C::TILE_BYTES : 0u;   // stream's slot in a stage
     const int col = lane & 31;     // query within the wave's 32
     const int half = lane >> 5;    // which 8-element k group of the MFMA operands
 
     int bh, qt;
     tile_of_block(blockIdx.x, gridDim.x, n_qtiles, CAUSAL, bh, qt);
-    const int q0 = qt * BM;
+    const int q0 = qt * BMQ;
     const int off = Nk - Nq;       // causal: key j visible to query i iff j <= i + off
 
     const u16* Qh = Q + (size_t)bh * Nq * D;
@@ -148,7 +164,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
 
     // ---- a1: Q fragment for this lane's query, all of d, kept in registers.
     // Rows past Nq read as zeros (buffer bounds) and are never stored.
-    const int qrow = q0 + wave * 32 + col;
+    const int qrow = q0 + qw * 32 + col;
     bf16x8 qf[D / 16];
     {
         const auto rq = make_rsrc(Qh, (uint32_t)Nq * RB);
@@ -160,37 +176,44 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         }
     }
 
-    // Key tiles this workgroup needs, and those this wave needs.
+    // Key tiles of this workgroup, of this wave's stream, and of this wave.
     int kv_end = Nk;
-    if (CAUSAL) kv_end = min(Nk, q0 + BM + off);
+    if (CAUSAL) kv_end = min(Nk, q0 + BMQ + off);
     const int n_kt = (kv_end + BN - 1) / BN;
-    const int wave_q_first = q0 + wave * 32;
-    int n_w = n_kt;
-    if (CAUSAL) n_w = min(n_kt, (wave_q_first + 31 + off) / BN + 1);
+    const int n_first = KSPLIT ? (n_kt + 1) / 2 : n_kt;      // tiles of stream 0
+    const int g_start = (KSPLIT && grp == 1) ? n_first : 0;   // first global tile of the stream
+    const int g_count = (KSPLIT && grp == 1) ? n_kt - n_first : n_first;
+    const int n_iter = n_first;                               // slots every wave walks through
+    const int wave_q_first = q0 + qw * 32;
+    int w_end = n_kt;                                         // global tiles this wave needs
+    if (CAUSAL) w_end = min(n_kt, (wave_q_first + 31 + off) / BN + 1);
+    const int n_w = max(0, min(g_start + g_count, w_end) - g_start);   // local count
 
-    // ---- a2: direct-to-LDS tile loads.  Lane l of the wave's i-th load fills
-    // LDS slot S = (wave*L + i)*64 + l, which holds logical chunk
-    // (S % CHUNKS) ^ swz(row) of row S / CHUNKS.
-    uint32_t ld_voff[C::LOADS_PER_WAVE];
+    // ---- a2: direct-to-LDS tile loads.  Lane l of the i-th load of loader lw
+    // fills slot S = (lw*LPW + i)*64 + l of its stream's tile, which holds
+    // logical chunk (S % CHUNKS) ^ swz(row) of row S / CHUNKS.
+    uint32_t ld_voff[LPW];
 #pragma unroll
-    for (int i = 0; i < C::LOADS_PER_WAVE; ++i) {
-        const int slot = (wave * C::LOADS_PER_WAVE + i) * 64 + lane;
+    for (int i = 0; i < LPW; ++i) {
+        const int slot = (lw * LPW + i) * 64 + lane;
         const int row = slot / C::CHUNKS, p = slot % C::CHUNKS;
         ld_voff[i] = (uint32_t)row * RB + (uint32_t)((p ^ swz<D>(row)) * 16);
     }
-    auto issue_tile_load = [&](const u16* head, int kbase, unsigned char* stage) {
+    // Loads the stream's local tile t into `stage` (only while t < g_count).
+    auto issue_tile_load = [&](const u16* head, int t, unsigned char* stage) {
+        const int kbase = (g_start + t) * BN;
         const auto r = make_rsrc(head + (size_t)kbase * D, (uint32_t)(Nk - kbase) * RB);
 #pragma unroll
-        for (int i = 0; i < C::LOADS_PER_WAVE; ++i)
-            buffer_load16_to_lds(r, stage + (wave * C::LOADS_PER_WAVE + i) * 1024, ld_voff[i]);
+        for (int i = 0; i < LPW; ++i)
+            buffer_load16_to_lds(r, stage + g_off + (lw * LPW + i) * 1024, ld_voff[i]);
     };
 
     // Per-lane LDS addresses of the MFMA operand reads (stage, key block and
-    // key chunk are added as immediates).
+    // key chunk are added as immediates; the stream's slot is folded in).
     uint32_t kaddr[D / 16];          // K rows: row = col (+32 kb), chunk 2s + half
 #pragma unroll
     for (int s = 0; s < D / 16; ++s)
-        kaddr[s] = (uint32_t)col * RB + (uint32_t)(((2 * s + half) ^ swz<D>(col)) * 16);
+        kaddr[s] = g_off + (uint32_t)col * RB + (uint32_t)(((2 * s + half) ^ swz<D>(col)) * 16);
     uint32_t vaddr[D / 32][2];       // V rows for ds_read_b64_tr_b16 (lo / hi key quads)
     {
         const int g = lane >> 4, j = (lane >> 2) & 3, q = lane & 3;
@@ -200,11 +223,10 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             for (int h8 = 0; h8 < 2; ++h8) {
                 const int row = 4 * (g >> 1) + j + 8 * h8;
                 const int dv = dv_of<D>(b, 16 * (g & 1) + 4 * q);
-                vaddr[b][h8] = (uint32_t)row * RB + (uint32_t)((((dv >> 3) ^ swz<D>(row)) * 16) +
-                                                               (dv & 7) * 2);
+                vaddr[b][h8] = g_off + (uint32_t)row * RB +
+                               (uint32_t)((((dv >> 3) ^ swz<D>(row)) * 16) + (dv & 7) * 2);
             }
     }
-
     f32x16 oacc[D / 32];
 #pragma unroll
     for (int b = 0; b < D / 32; ++b) oacc[b] = f32x16{};
@@ -284,7 +306,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     auto softmax_full = [&](int t, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
         if constexpr (MASK) {
-            const int kbase = t * BN;
+            const int kbase = (g_start + t) * BN;
 #pragma unroll
             for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
@@ -303,8 +325,11 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         const float mt = (MASK && mx == kNegInf) ? kNegInf : mx * c;
         const bool need = wave_any(mt > m_run + kRescaleSlack);
         if (need) {
+            // A row may have seen no visible key yet (its reference is still
+            // -inf, e.g. the second key stream of a causal workgroup): there is
+            // nothing to rescale, and 2^(-inf - -inf) must not be formed.
             const float m_new = fmaxf(m_run, mt);
-            const float alpha = exp2_hw(m_run - m_new);
+            const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
             l_run *= alpha;
             alpha_pend = rescale_pend ? alpha_pend * alpha : alpha;
             rescale_pend = true;
@@ -324,7 +349,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         else l_run += part;
     };
     auto tile_needs_mask = [&](int t) {
-        const int kbase = t * BN;
+        const int kbase = (g_start + t) * BN;
         return (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
     };
 
@@ -342,40 +367,71 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     };
     auto softmax_phase = [&](int t) {
         if (t < n_w) {
-            if (tile_needs_mask(t) || m_run == kNegInf) softmax_full(t, std::true_type{});
+            if (tile_needs_mask(t) || wave_any(m_run == kNegInf)) softmax_full(t, std::true_type{});
             else softmax_fast(t);
         }
     };
 
-    // Phases u = 0, 1, 2, ...: the leading group runs gemm(t) in phase 2t and
-    // softmax(t) in phase 2t + 1; the trailing group runs gemm(t) in phase
-    // 2t + 1 and softmax(t) in phase 2t + 2.  K(t+1) and V(t) are loaded during
-    // phases 2t and 2t + 1 into the stages freed by phase 2t - 1.
-    issue_tile_load(Kh, 0, k_st0);
+    // Slots t = 0, 1, 2, ... over the stream's local tiles.  Ping-pong: the
+    // leading group runs gemm(t) in the first half of slot t and softmax(t) in
+    // the second; the trailing group runs softmax(t-1), then gemm(t).  Key
+    // split: every wave leads.  K(t+1) and V(t) are loaded during slot t into
+    // the stages freed by slot t - 1.
+    const bool lead = KSPLIT || grp == 0;
+    if (g_count > 0) issue_tile_load(Kh, 0, k_st0);
     wait_loads_to_lds();
     __syncthreads();
-    for (int t = 0; t <= n_kt; t += 2) {
+    for (int t = 0; t <= n_iter; t += 2) {
         // ---- even tile t (parity 0)
-        if (t + 1 < n_kt) issue_tile_load(Kh, (t + 1) * BN, k_st1);
-        if (t < n_kt) issue_tile_load(Vh, t * BN, v_st0);
-        if (grp == 0) gemm_phase(t, std::integral_constant<int, 0>{});
+        if (t + 1 < g_count) issue_tile_load(Kh, t + 1, k_st1);
+        if (t < g_count) issue_tile_load(Vh, t, v_st0);
+        if (lead) gemm_phase(t, S0{});
         else if (t >= 1) softmax_phase(t - 1);
-        __syncthreads();
-        if (grp == 0) softmax_phase(t);
-        else gemm_phase(t, std::integral_constant<int, 0>{});
+        if constexpr (!KSPLIT) __syncthreads();
+        if (lead) softmax_phase(t);
+        else gemm_phase(t, S0{});
         wait_loads_to_lds();
         __syncthreads();
-        if (t + 1 > n_kt) break;
+        if (t + 1 > n_iter) break;
         // ---- odd tile t + 1 (parity 1)
-        if (t + 2 < n_kt) issue_tile_load(Kh, (t + 2) * BN, k_st0);
-        if (t + 1 < n_kt) issue_tile_load(Vh, (t + 1) * BN, v_st1);
-        if (grp == 0) gemm_phase(t + 1, std::integral_constant<int, 1>{});
+        if (t + 2 < g_count) issue_tile_load(Kh, t + 2, k_st0);
+        if (t + 1 < g_count) issue_tile_load(Vh, t + 1, v_st1);
+        if (lead) gemm_phase(t + 1, S1{});
         else softmax_phase(t);
-        __syncthreads();
-        if (grp == 0) softmax_phase(t + 1);
-        else gemm_phase(t + 1, std::integral_constant<int, 1>{});
+        if constexpr (!KSPLIT) __syncthreads();
+        if (lead) softmax_phase(t + 1);
+        else gemm_phase(t + 1, S1{});
         wait_loads_to_lds();
         __syncthreads();
+    }
+
+    // Key split: group 1 hands (m, l, O^T) to group 0, which merges exactly:
+    // M = max(m0, m1), O = 2^(m0-M) O0 + 2^(m1-M) O1, l likewise.  The K ring
+    // holds the O^T blocks ([reg][lane], lane-contiguous), the V ring m and l.
+    if constexpr (KSPLIT) {
+        float* xo = reinterpret_cast<float*>((qw < 2 ? k_st0 : k_st1) +
+                                             (qw & 1) * (D / 2) * 64 * sizeof(float));
+        float* xml = reinterpret_cast<float*>(v_st0) + qw * 2 * 64;
+        if (grp == 1) {
+#pragma unroll
+            for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) xo[(b * 16 + i) * 64 + lane] = oacc[b][i];
+            xml[lane] = m_run;
+            xml[64 + lane] = l_run;
+        }
+        __syncthreads();
+        if (grp == 1) return;
+        const float m1 = xml[lane], l1 = xml[64 + lane];
+        const float mm = fmaxf(m_run, m1);
+        const float a0 = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - mm);
+        const float a1 = (m1 == kNegInf) ? 0.0f : exp2_hw(m1 - mm);
+        l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+        for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) oacc[b][i] = oacc[b][i] * a0 + xo[(b * 16 + i) * 64 + lane] * a1;
+        m_run = mm;
     }
 
     // ---- a7: epilogue, O = acc / l: the only device-memory write.
@@ -404,15 +460,26 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     }
 }
 
+// Workgroups below which the ping-pong grid leaves CUs idle for long: below it
+// the key-split layout (half the queries per workgroup, two key streams) is
+// launched instead, doubling the workgroups.
+constexpr long long kKeySplitBelowBlocks = 1024;
+
 template <int D, bool CAUSAL, bool OUT_BF16>
 hipError_t launch(const Problem& p, hipStream_t stream) {
-    const int n_qtiles = (p.nq + BM - 1) / BM;
-    const long long blocks = (long long)p.bh * n_qtiles;
     const float c = p.scale * kLog2e;
-    return launch_kernel(prefill_bf16_kernel<D, CAUSAL, OUT_BF16>, dim3((unsigned)blocks),
-                         dim3(THREADS), stream, static_cast<const u16*>(p.q),
-                         static_cast<const u16*>(p.k), static_cast<const u16*>(p.v), p.o, p.lse,
-                         p.nq, p.nk, n_qtiles, c);
+    const int qt_pp = (p.nq + BM - 1) / BM;
+    if ((long long)p.bh * qt_pp >= kKeySplitBelowBlocks || p.nk <= BN) {
+        return launch_kernel(prefill_bf16_kernel<D, CAUSAL, OUT_BF16, false>,
+                             dim3((unsigned)((long long)p.bh * qt_pp)), dim3(THREADS), stream,
+                             static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
+                             static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, qt_pp, c);
+    }
+    const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
+    return launch_kernel(prefill_bf16_kernel<D, CAUSAL, OUT_BF16, true>,
+                         dim3((unsigned)((long long)p.bh * qt_ks)), dim3(THREADS), stream,
+                         static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
+                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, qt_ks, c);
 }
 
 template <int D>

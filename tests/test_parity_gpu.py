@@ -62,6 +62,31 @@ def _lse_tol(dtype, ref_lse):
     return 4e-3 + 1e-5 * np.abs(ref_lse).max()
 
 
+# Grids of >= 1024 workgroups of 256 queries take the ping-pong layout; the
+# smaller prefill shapes above take the key-split layout.  These cover the
+# ping-pong layout with ragged query and key tails, on sampled rows.
+PINGPONG_SHAPES = [
+    # B, H, Nq, Nk, d
+    (4, 64, 1000, 1000, 64),
+    (2, 128, 1000, 1100, 128),
+    (1, 256, 1024, 1024, 128),
+]
+
+
+@pytest.mark.parametrize("shape", PINGPONG_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_prefill_pingpong_layout_sampled(shape, causal):
+    B, H, Nq, Nk, d = shape
+    say(f"prefill ping-pong {shape} causal={causal}")
+    q, k, v = gen(B, H, Nq, Nk, d, "bf16", seed=_seed("pp", shape, causal))
+    o = run_gpu(q, k, v, causal=causal, out_dtype="f32")
+    rows = sample_rows(B, H, Nq, 256, seed=3, tile=256)
+    ref = oracle.attention_rows(q, k, v, rows, causal=causal)
+    err = max_err(o.reshape(-1, d)[rows], ref)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
 DECODE_CASES = [
     # B, H, Nk, d, splits
     (1, 1, 1, 64, 0),
