@@ -38,6 +38,8 @@
 // accumulated against the stale maximum.  The final O = acc / l uses the same
 // reference for numerator and denominator, so the result is the same softmax
 // (Steps I-IV regrouped over key tiles).
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "device_common.h"
@@ -85,18 +87,24 @@ __device__ __forceinline__ int dv_of(int b, int m) {
     return 32 * b + m;
 }
 
-// Workgroup index -> (head slice, query tile), keeping the query tiles of one
-// head on one XCD (workgroups are handed to the 8 XCDs round-robin) so that
-// the K/V tiles they all stream are shared in that XCD's L2.  Within a head
-// the heaviest causal tiles start first.
-__device__ __forceinline__ void tile_of_block(int bid, int nblocks, int n_qtiles, bool causal,
-                                              int& bh, int& qt) {
-    const int per = nblocks >> 3, rem = nblocks & 7;
-    const int x = bid & 7, r = bid >> 3;
-    const int logical = x * per + (x < rem ? x : rem) + r;
-    bh = logical / n_qtiles;
-    const int t = logical - bh * n_qtiles;
-    qt = causal ? (n_qtiles - 1 - t) : t;
+// Persistent schedule.  The grid holds as many workgroups as the GPU runs at
+// once (P); workgroup p walks its share of the n_bh * n_qtiles work items
+// (head slice, query tile) and returns when it has none left, so no workgroup
+// is ever dispatched behind a busy one.  Items are ranked query tile by query
+// tile, all head slices of a rank together.  Without a causal mask every item
+// costs the same and workgroup p takes items p, P + p, 2P + p, ...: with P a
+// multiple of n_bh it keeps one head slice throughout.  With the mask, tiles
+// cost in proportion to their row index: ranks run from the last query tile
+// down and the deal snakes (p, 2P - 1 - p, 2P + p, ...), so every workgroup
+// pairs a heavy item with a light one.
+__device__ __forceinline__ bool item_of(int p, int i, int P, int n_bh, int n_qtiles, bool causal,
+                                        int& bh, int& qt) {
+    const long long j = (long long)i * P + ((causal && (i & 1)) ? P - 1 - p : p);
+    if (j >= (long long)n_bh * n_qtiles) return false;
+    const int rank = (int)(j / n_bh);
+    bh = (int)(j - (long long)rank * n_bh);
+    qt = causal ? n_qtiles - 1 - rank : rank;
+    return true;
 }
 
 __device__ __forceinline__ void wait_loads_to_lds() {
@@ -113,7 +121,7 @@ __device__ __forceinline__ void wait_loads_to_lds() {
 template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT>
 __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
-    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
+    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c) {
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
     constexpr int NG = KSPLIT ? 2 : 1;                    // independent key streams
@@ -148,19 +156,20 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const int col = lane & 31;     // query within the wave's 32
     const int half = lane >> 5;    // which 8-element k group of the MFMA operands
 
-    int bh, qt;
-    tile_of_block(blockIdx.x, gridDim.x, n_qtiles, CAUSAL, bh, qt);
-    const int q0 = qt * BMQ;
     const int off = Nk - Nq;       // causal: key j visible to query i iff j <= i + off
-
-    const u16* Qh = Q + (size_t)bh * Nq * D;
-    const u16* Kh = K + (size_t)bh * Nk * D;
-    const u16* Vh = V + (size_t)bh * Nk * D;
-
     // A negative scale is folded into Q's sign (exact for bf16) so that the
     // softmax below always sees c >= 0.
     const uint32_t qflip = (c < 0.0f) ? 0x80008000u : 0u;
     c = fabsf(c);
+
+    for (int item = 0;; ++item) {
+    int bh, qt;
+    if (!item_of(blockIdx.x, item, gridDim.x, n_bh, n_qtiles, CAUSAL, bh, qt)) break;
+    const int q0 = qt * BMQ;
+
+    const u16* Qh = Q + (size_t)bh * Nq * D;
+    const u16* Kh = K + (size_t)bh * Nk * D;
+    const u16* Vh = V + (size_t)bh * Nk * D;
 
     // ---- a1: Q fragment for this lane's query, all of d, kept in registers.
     // Rows past Nq read as zeros (buffer bounds) and are never stored.
@@ -421,7 +430,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             xml[64 + lane] = l_run;
         }
         __syncthreads();
-        if (grp == 1) return;
+        if (grp == 0) {
         const float m1 = xml[lane], l1 = xml[64 + lane];
         const float mm = fmaxf(m_run, m1);
         const float a0 = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - mm);
@@ -432,9 +441,12 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
 #pragma unroll
             for (int i = 0; i < 16; ++i) oacc[b][i] = oacc[b][i] * a0 + xo[(b * 16 + i) * 64 + lane] * a1;
         m_run = mm;
+        }
     }
 
-    // ---- a7: epilogue, O = acc / l: the only device-memory write.
+    // ---- a7: epilogue, O = acc / l: the only device-memory write (key
+    // split: by group 0, which holds the merged state).
+    if (!KSPLIT || grp == 0) {
     const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
     if (qrow < Nq) {
@@ -458,28 +470,62 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         if (LSE != nullptr && half == 0)
             LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
     }
+    }
+    // Every wave is done with this item's LDS before the next item's first
+    // tile load lands there.
+    __syncthreads();
+    }
 }
 
-// Workgroups below which the ping-pong grid leaves CUs idle for long: below it
-// the key-split layout (half the queries per workgroup, two key streams) is
-// launched instead, doubling the workgroups.
-constexpr long long kKeySplitBelowBlocks = 1024;
+// Work items below which the ping-pong layout leaves CUs idle for long: below
+// it the key-split layout (half the queries per item, two key streams) is
+// launched instead, doubling the items.
+constexpr long long kKeySplitBelowItems = 1024;
+
+// Compute units of the device that runs `stream` (cached per device).
+hipError_t device_cus(hipStream_t stream, int& cus) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices];
+    hipDevice_t dev = 0;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < kMaxDevices && (cus = cache[dev].load(std::memory_order_relaxed)) > 0)
+        return hipSuccess;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    if (cus < 1) cus = 1;
+    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(cus, std::memory_order_relaxed);
+    return hipSuccess;
+}
+
+// One persistent launch: as many workgroups as the device holds at once, at
+// most one per work item.
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT>
+hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, hipStream_t stream) {
+    auto kernel = prefill_bf16_kernel<D, CAUSAL, OUT_BF16, KSPLIT>;
+    static const int per_cu = [&] {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, THREADS, 0) != hipSuccess) n = 1;
+        return n > 0 ? n : 1;
+    }();
+    int cus = 0;
+    const hipError_t e = device_cus(stream, cus);
+    if (e != hipSuccess) return e;
+    const long long items = (long long)p.bh * n_qtiles;
+    const unsigned grid = (unsigned)std::min<long long>(items, (long long)cus * per_cu);
+    return launch_kernel(kernel, dim3(grid), dim3(THREADS), stream,
+                         static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
+                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, p.bh, n_qtiles, c);
+}
 
 template <int D, bool CAUSAL, bool OUT_BF16>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const float c = p.scale * kLog2e;
     const int qt_pp = (p.nq + BM - 1) / BM;
-    if ((long long)p.bh * qt_pp >= kKeySplitBelowBlocks || p.nk <= BN) {
-        return launch_kernel(prefill_bf16_kernel<D, CAUSAL, OUT_BF16, false>,
-                             dim3((unsigned)((long long)p.bh * qt_pp)), dim3(THREADS), stream,
-                             static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
-                             static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, qt_pp, c);
-    }
+    if ((long long)p.bh * qt_pp >= kKeySplitBelowItems || p.nk <= BN)
+        return launch_persistent<D, CAUSAL, OUT_BF16, false>(p, qt_pp, c, stream);
     const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
-    return launch_kernel(prefill_bf16_kernel<D, CAUSAL, OUT_BF16, true>,
-                         dim3((unsigned)((long long)p.bh * qt_ks)), dim3(THREADS), stream,
-                         static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
-                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, qt_ks, c);
+    return launch_persistent<D, CAUSAL, OUT_BF16, true>(p, qt_ks, c, stream);
 }
 
 template <int D>
