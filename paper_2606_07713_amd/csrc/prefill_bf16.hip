@@ -158,9 +158,11 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
 
     const int off = Nk - Nq;       // causal: key j visible to query i iff j <= i + off
     // A negative scale is folded into Q's sign (exact for bf16) so that the
-    // softmax below always sees c >= 0.
+    // softmax below always sees c > 0.  A zero (or denormal) scale becomes the
+    // smallest normal float: every weight still rounds to exactly 1, and a
+    // masked score (-inf) still gives weight 0 rather than -inf * 0 = NaN.
     const uint32_t qflip = (c < 0.0f) ? 0x80008000u : 0u;
-    c = fabsf(c);
+    c = fmaxf(fabsf(c), 1.17549435e-38f);
 
     for (int item = 0;; ++item) {
     int bh, qt;
@@ -285,58 +287,62 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // Weights are p = 2^(s c - m) against the running reference m, rounded to
     // bf16 for the P.V product; the denominator sums exactly those rounded
     // weights (v_dot2_f32_bf16 against ones), so numerator and denominator use
-    // the same p.  exp_pack() returns the tile's partial sum.
-    auto exp_pack = [&](float neg_m, auto mask_tag) {
-        constexpr bool MASK = decltype(mask_tag)::value;
+    // the same p.  exp_pack() returns the tile's partial sum (this lane's 32
+    // keys).  Masked scores are -inf and c > 0, so their weight is exactly 0.
+    auto exp_pack = [&](float neg_m) {
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
         float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                float p0 = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
-                float p1 = exp2_hw(__builtin_fmaf(sacc[kb][i + 1], c, neg_m));
-                if constexpr (MASK) {
-                    p0 = (sacc[kb][i] == kNegInf) ? 0.0f : p0;
-                    p1 = (sacc[kb][i + 1] == kNegInf) ? 0.0f : p1;
+            for (int g = 0; g < 2; ++g) {
+                u32x4 w;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int i = g * 8 + 2 * j;
+                    const float p0 = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
+                    const float p1 = exp2_hw(__builtin_fmaf(sacc[kb][i + 1], c, neg_m));
+                    const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
+                    w[j] = __builtin_bit_cast(uint32_t, pp);
+                    part[j] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, part[j], false);
                 }
-                const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
-                pbuf[kb * 2 + (i >> 3)][i & 7] = pp[0];
-                pbuf[kb * 2 + (i >> 3)][(i & 7) + 1] = pp[1];
-                part[(i >> 1) & 3] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, part[(i >> 1) & 3], false);
+                pbuf[kb * 2 + g] = __builtin_bit_cast(bf16x8, w);
             }
         return (part[0] + part[1]) + (part[2] + part[3]);
     };
 
-    // Full step: tile max (Step I), raise the reference when it outgrew the
-    // slack, then the weights.  Used for masked tiles and whenever the fast
-    // step's check fails.
-    auto softmax_full = [&](int t, auto mask_tag) {
-        constexpr bool MASK = decltype(mask_tag)::value;
-        if constexpr (MASK) {
-            const int kbase = (g_start + t) * BN;
+    // Causal / ragged tiles: scores of keys this query must not see become
+    // -inf in place.
+    auto apply_mask = [&](int t) {
+        const int kbase = (g_start + t) * BN;
 #pragma unroll
-            for (int kb = 0; kb < BN / 32; ++kb)
+        for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = kbase + kb * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
-                    const bool masked = key >= Nk || (CAUSAL && key > qrow + off);
-                    if (masked) sacc[kb][i] = kNegInf;
-                }
-        }
+            for (int i = 0; i < 16; ++i) {
+                const int key = kbase + kb * 32 + (i >> 2) * 8 + half * 4 + (i & 3);
+                const bool masked = key >= Nk || (CAUSAL && key > qrow + off);
+                if (masked) sacc[kb][i] = kNegInf;
+            }
+    };
+
+    // Step I on the tile: its row max; the reference is raised (and l, O owe
+    // the factor 2^(m_old - m_new)) only when the tile exceeds it by more than
+    // kRescaleSlack.
+    auto raise_reference = [&]() {
+        // The empty asm keeps the max from being hoisted onto the fast path
+        // (the scores do not change between the passes below).
         float mx = kNegInf;
+        asm volatile("" : "+v"(mx));
 #pragma unroll
         for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
-        mx = half_max(mx);
-        const float mt = (MASK && mx == kNegInf) ? kNegInf : mx * c;
-        const bool need = wave_any(mt > m_run + kRescaleSlack);
-        if (need) {
+        const float mt = half_max(mx) * c;
+        if (wave_any(mt > m_run + kRescaleSlack)) {
             // A row may have seen no visible key yet (its reference is still
-            // -inf, e.g. the second key stream of a causal workgroup): there is
-            // nothing to rescale, and 2^(-inf - -inf) must not be formed.
+            // -inf): there is nothing to rescale, and 2^(-inf - -inf) must
+            // not be formed.
             const float m_new = fmaxf(m_run, mt);
             const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
             l_run *= alpha;
@@ -344,22 +350,34 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             rescale_pend = true;
             m_run = m_new;
         }
-        l_run += exp_pack(-m_run, mask_tag);
     };
 
-    // Fast step for interior tiles: no max.  The weights are taken against
-    // the current reference directly; if any tile's partial sum exceeds
-    // 2^kFastSumLimit (or overflowed), the tile is redone by the full step.
-    // Any reference gives the same quotient, so this is exact; it only skips
-    // Step I's max while the reference is still close enough to it.
-    auto softmax_fast = [&](int t) {
-        const float part = exp_pack(-m_run, std::false_type{});
-        if (wave_any(!(part <= kFastSumLimit))) softmax_full(t, std::false_type{});
-        else l_run += part;
-    };
     auto tile_needs_mask = [&](int t) {
         const int kbase = (g_start + t) * BN;
         return (kbase + BN > Nk) || (CAUSAL && kbase + BN - 1 > wave_q_first + off);
+    };
+
+    // Softmax of tile t.  The weights are first taken against the current
+    // reference without computing the tile max; only if a partial sum exceeds
+    // kFastSumLimit (or overflowed) is the reference raised and the tile
+    // redone.  Any reference gives the same quotient, so this is exact.  A
+    // row that has seen no key yet starts from its tile max instead (a guessed
+    // reference far above its scores would underflow every weight); rows
+    // still without a visible key take reference 0, all their scores being
+    // -inf.  The pass loop
+    // is not unrolled so that pbuf has a single producer.
+    auto softmax_phase = [&](int t) {
+        if (t >= n_w) return;
+        if (tile_needs_mask(t)) apply_mask(t);
+        if (wave_any(m_run == kNegInf)) raise_reference();
+        float part;
+#pragma clang loop unroll(disable)
+        for (int pass = 0;; ++pass) {
+            part = exp_pack(m_run == kNegInf ? 0.0f : -m_run);
+            if (pass == 1 || !wave_any(!(part <= kFastSumLimit))) break;
+            raise_reference();
+        }
+        l_run += part;
     };
 
     // Matrix phase of tile t: P(t-1) V(t-1) then S(t).  K(t) sits in K stage
@@ -373,12 +391,6 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         }
         if (t >= 1 && t - 1 < n_w) pv_mfma(std::integral_constant<int, 1 - P>{});
         if (t < n_w) s_mfma(std::integral_constant<int, P>{});
-    };
-    auto softmax_phase = [&](int t) {
-        if (t < n_w) {
-            if (tile_needs_mask(t) || wave_any(m_run == kNegInf)) softmax_full(t, std::true_type{});
-            else softmax_fast(t);
-        }
     };
 
     // Slots t = 0, 1, 2, ... over the stream's local tiles.  Ping-pong: the
