@@ -39,73 +39,18 @@
 // reference for numerator and denominator, so the result is the same softmax
 // (Steps I-IV regrouped over key tiles).
 #include <algorithm>
-#include <atomic>
 #include <type_traits>
 
 #include "device_common.h"
 #include "launch.h"
+#include "prefill_bf16_common.h"
 
 namespace moa {
 namespace {
 
-constexpr int WAVES = 8;         // two groups of four; wave w and w + 4 share a SIMD
-constexpr int THREADS = WAVES * 64;
+using namespace pf;
+
 constexpr int BM = WAVES * 32;   // queries per workgroup (ping-pong layout)
-constexpr int BN = 64;           // keys per tile
-constexpr float kRescaleSlack = 8.0f;
-constexpr float kFastSumLimit = 1048576.0f;   // 2^20
-
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4s lds_v4s;
-
-template <int D>
-struct Cfg {
-    static constexpr int CHUNKS = D / 8;                        // 16-byte chunks per row
-    static constexpr uint32_t ROW_BYTES = D * 2;
-    static constexpr uint32_t TILE_BYTES = BN * ROW_BYTES;      // one K or V tile
-    static constexpr int LOADS_PER_WAVE = TILE_BYTES / (WAVES * 1024);
-    static_assert(TILE_BYTES % (WAVES * 1024) == 0, "tile must split into wave loads");
-};
-
-// 16-byte-chunk XOR swizzle of LDS row `row` (a permutation of the row's
-// chunks).  With 64 four-byte banks: the K operand reads (16 lanes, 16
-// consecutive rows, one logical chunk) hit 16 distinct bank groups, and the
-// transposing V reads (32 lanes: 4 rows x 2 chunks x 2 halves per 16 lanes)
-// hit 64 distinct banks -- for d = 128 together with the dv order below.
-template <int D>
-__device__ __forceinline__ int swz(int row) {
-    if constexpr (D == 128) return ((row & 3) << 1) | (((row >> 2) & 1) << 3) | ((row >> 3) & 1);
-    return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
-}
-
-// dv index held by row m (0..31) of the b-th O^T accumulator block.  For d =
-// 128 the two 16-row halves of a block take dv ranges 64 apart, so the two
-// 16-lane groups of a transposing read touch opposite bank halves.
-template <int D>
-__device__ __forceinline__ int dv_of(int b, int m) {
-    if constexpr (D == 128) return (m < 16) ? 16 * b + m : 64 + 16 * b + (m - 16);
-    return 32 * b + m;
-}
-
-// Persistent schedule.  The grid holds as many workgroups as the GPU runs at
-// once (P); workgroup p walks its share of the n_bh * n_qtiles work items
-// (head slice, query tile) and returns when it has none left, so no workgroup
-// is ever dispatched behind a busy one.  Items are ranked query tile by query
-// tile, all head slices of a rank together.  Without a causal mask every item
-// costs the same and workgroup p takes items p, P + p, 2P + p, ...: with P a
-// multiple of n_bh it keeps one head slice throughout.  With the mask, tiles
-// cost in proportion to their row index: ranks run from the last query tile
-// down and the deal snakes (p, 2P - 1 - p, 2P + p, ...), so every workgroup
-// pairs a heavy item with a light one.
-__device__ __forceinline__ bool item_of(int p, int i, int P, int n_bh, int n_qtiles, bool causal,
-                                        int& bh, int& qt) {
-    const long long j = (long long)i * P + ((causal && (i & 1)) ? P - 1 - p : p);
-    if (j >= (long long)n_bh * n_qtiles) return false;
-    const int rank = (int)(j / n_bh);
-    bh = (int)(j - (long long)rank * n_bh);
-    qt = causal ? n_qtiles - 1 - rank : rank;
-    return true;
-}
 
 __device__ __forceinline__ void wait_loads_to_lds() {
     __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's LDS-bound loads have landed
@@ -489,26 +434,11 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     }
 }
 
-// Work items below which the ping-pong layout leaves CUs idle for long: below
-// it the key-split layout (half the queries per item, two key streams) is
-// launched instead, doubling the items.
-constexpr long long kKeySplitBelowItems = 1024;
-
-// Compute units of the device that runs `stream` (cached per device).
-hipError_t device_cus(hipStream_t stream, int& cus) {
-    constexpr int kMaxDevices = 64;
-    static std::atomic<int> cache[kMaxDevices];
-    hipDevice_t dev = 0;
-    hipError_t e = hipStreamGetDevice(stream, &dev);
-    if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < kMaxDevices && (cus = cache[dev].load(std::memory_order_relaxed)) > 0)
-        return hipSuccess;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
-    if (cus < 1) cus = 1;
-    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(cus, std::memory_order_relaxed);
-    return hipSuccess;
-}
+// Layout choice by the number of 256-query work items.  From
+// kPingPongFromItems on, the ping-pong layout is the fastest measured; from
+// one item per compute unit on, the per-wave pipelined kernel; below that the
+// key-split layout, which halves the queries per item to double the items.
+constexpr long long kPingPongFromItems = 1024;
 
 // One persistent launch: as many workgroups as the device holds at once, at
 // most one per work item.
@@ -534,8 +464,13 @@ template <int D, bool CAUSAL, bool OUT_BF16>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const float c = p.scale * kLog2e;
     const int qt_pp = (p.nq + BM - 1) / BM;
-    if ((long long)p.bh * qt_pp >= kKeySplitBelowItems || p.nk <= BN)
+    const long long items = (long long)p.bh * qt_pp;
+    if (items >= kPingPongFromItems || p.nk <= BN)
         return launch_persistent<D, CAUSAL, OUT_BF16, false>(p, qt_pp, c, stream);
+    int cus = 0;
+    const hipError_t e = device_cus(stream, cus);
+    if (e != hipSuccess) return e;
+    if (items >= cus) return launch_prefill_bf16_pipe(p, stream);
     const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
     return launch_persistent<D, CAUSAL, OUT_BF16, true>(p, qt_ks, c, stream);
 }

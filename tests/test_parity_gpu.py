@@ -62,9 +62,11 @@ def _lse_tol(dtype, ref_lse):
     return 4e-3 + 1e-5 * np.abs(ref_lse).max()
 
 
-# Grids of >= 1024 workgroups of 256 queries take the ping-pong layout; the
-# smaller prefill shapes above take the key-split layout.  These cover the
-# ping-pong layout with ragged query and key tails, on sampled rows.
+# Grids of >= 1024 work items of 256 queries take the ping-pong layout, grids
+# of at least one item per compute unit (256 on MI355X) the per-wave pipelined
+# kernel, and the smaller prefill shapes above the key-split layout.  These
+# cover the two larger layouts with ragged query and key tails, on sampled
+# rows.
 PINGPONG_SHAPES = [
     # B, H, Nq, Nk, d
     (4, 64, 1000, 1000, 64),
@@ -84,6 +86,43 @@ def test_prefill_pingpong_layout_sampled(shape, causal):
     ref = oracle.attention_rows(q, k, v, rows, causal=causal)
     err = max_err(o.reshape(-1, d)[rows], ref)
     say(f"  max err {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
+PIPE_SHAPES = [
+    # B, H, Nq, Nk, d   (256 <= B*H*ceil(Nq/256) < 1024)
+    (2, 64, 1000, 1000, 64),
+    (1, 128, 600, 700, 128),
+    (4, 16, 1024, 1024, 128),
+    (1, 96, 2000, 2000, 128),
+]
+
+
+@pytest.mark.parametrize("shape", PIPE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_prefill_pipe_layout_sampled(shape, causal):
+    B, H, Nq, Nk, d = shape
+    say(f"prefill pipelined {shape} causal={causal}")
+    q, k, v = gen(B, H, Nq, Nk, d, "bf16", seed=_seed("pipe", shape, causal))
+    o, lse = run_gpu(q, k, v, causal=causal, out_dtype="f32", return_lse=True)
+    rows = sample_rows(B, H, Nq, 256, seed=5, tile=256)
+    ref, ref_lse = oracle.attention_rows(q, k, v, rows, causal=causal, with_lse=True)
+    err = max_err(o.reshape(-1, d)[rows], ref)
+    lse_err = float(np.abs(lse.reshape(-1)[rows] - ref_lse).max())
+    say(f"  max err {err:.3e}  lse err {lse_err:.3e}")
+    assert err <= TOL["bf16"]
+    assert lse_err <= _lse_tol("bf16", ref_lse)
+
+
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_prefill_pipe_layout_bf16_out(causal):
+    B, H, Nq, Nk, d = (1, 128, 600, 700, 128)
+    q, k, v = gen(B, H, Nq, Nk, d, "bf16", seed=_seed("pipe-bf16", causal))
+    o = run_gpu(q, k, v, causal=causal, out_dtype="bf16")
+    rows = sample_rows(B, H, Nq, 256, seed=6, tile=256)
+    ref = oracle.attention_rows(q, k, v, rows, causal=causal)
+    err = max_err(o.reshape(-1, d)[rows], ref)
+    say(f"prefill pipelined bf16 out causal={causal}: max err {err:.3e}")
     assert err <= TOL["bf16"]
 
 
