@@ -21,12 +21,13 @@
 // once; two waves per SIMD interleave further.  There is no phase barrier
 // between waves.
 //
-// Data movement.  K and V go from device memory straight into LDS
-// (buffer_load ... lds) through 4-stage rings of 64-key tiles, three stages
-// ahead of use; each stage is its own LDS array so that reads of one stage
-// never wait for loads landing in another.  One barrier per 64 keys frees a
-// stage for reuse.  Loads past Nk (ragged tail, or stages beyond the item's
-// last) read zeros through the buffer bound.
+// Data movement.  K and V stages of 64 keys go from device memory into
+// registers (16 bytes per lane, coalesced; rows past Nk read as zeros through
+// the buffer bound) one stage iteration before they are stored into a
+// two-stage LDS ring, so a load has a whole iteration to arrive and the
+// compiler tracks it like any register load.  One barrier per 64 keys, without
+// the memory-model fences of __syncthreads(), publishes a stage and frees the
+// other.
 //
 // Softmax.  Scores stay in raw units; with c = scale * log2(e) the weight of
 // key j is 2^(s_j c - m) for a running reference m (log2 units) that is
