@@ -342,7 +342,10 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // leading group runs gemm(t) in the first half of slot t and softmax(t) in
     // the second; the trailing group runs softmax(t-1), then gemm(t).  Key
     // split: every wave leads.  K(t+1) and V(t) are loaded during slot t into
-    // the stages freed by slot t - 1.
+    // the stages freed by slot t - 1 and waited for at its end.  The barrier
+    // between the two halves of a slot only swaps the groups' roles: it
+    // guards no LDS data, so it carries no memory fence (which would wait for
+    // the loads in flight at mid-slot).
     const bool lead = KSPLIT || grp == 0;
     if (g_count > 0) issue_tile_load(Kh, 0, k_st0);
     wait_loads_to_lds();
@@ -353,7 +356,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         if (t < g_count) issue_tile_load(Vh, t, v_st0);
         if (lead) gemm_phase(t, S0{});
         else if (t >= 1) softmax_phase(t - 1);
-        if constexpr (!KSPLIT) __syncthreads();
+        if constexpr (!KSPLIT) barrier_no_fence();
         if (lead) softmax_phase(t);
         else gemm_phase(t, S0{});
         wait_loads_to_lds();
@@ -364,7 +367,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         if (t + 1 < g_count) issue_tile_load(Vh, t + 1, v_st1);
         if (lead) gemm_phase(t + 1, S1{});
         else softmax_phase(t);
-        if constexpr (!KSPLIT) __syncthreads();
+        if constexpr (!KSPLIT) barrier_no_fence();
         if (lead) softmax_phase(t + 1);
         else gemm_phase(t + 1, S1{});
         wait_loads_to_lds();
