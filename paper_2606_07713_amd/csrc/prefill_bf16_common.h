@@ -52,17 +52,30 @@ __device__ __forceinline__ int dv_of(int b, int m) {
 // (head slice, query tile) and returns when it has none left, so no workgroup
 // is ever dispatched behind a busy one.  Items are ranked query tile by query
 // tile, all head slices of a rank together.  Without a causal mask every item
-// costs the same and workgroup p takes items p, P + p, 2P + p, ...: with P a
-// multiple of n_bh it keeps one head slice throughout.  With the mask, tiles
-// cost in proportion to their row index: ranks run from the last query tile
+// costs the same and a workgroup takes every P-th item; with the mask, tiles
+// cost in proportion to their row index, ranks run from the last query tile
 // down and the deal snakes (p, 2P - 1 - p, 2P + p, ...), so every workgroup
 // pairs a heavy item with a light one.
+//
+// Workgroups reach the 8 XCDs round-robin (p on XCD p % 8) and each XCD has
+// its own L2.  When head slices and workgroups both split evenly over the
+// XCDs, the deal is done per XCD over the head slices h = x (mod 8), so each
+// XCD streams the K/V of only its own heads.
 __device__ __forceinline__ bool item_of(int p, int i, int P, int n_bh, int n_qtiles, bool causal,
                                         int& bh, int& qt) {
-    const long long j = (long long)i * P + ((causal && (i & 1)) ? P - 1 - p : p);
-    if (j >= (long long)n_bh * n_qtiles) return false;
-    const int rank = (int)(j / n_bh);
-    bh = (int)(j - (long long)rank * n_bh);
+    constexpr int kXcds = 8;
+    int pl = p, Pl = P, hl = n_bh, x = 0, hstride = 1;
+    if (n_bh % kXcds == 0 && P % kXcds == 0) {
+        x = p % kXcds;
+        pl = p / kXcds;
+        Pl = P / kXcds;
+        hl = n_bh / kXcds;
+        hstride = kXcds;
+    }
+    const long long j = (long long)i * Pl + ((causal && (i & 1)) ? Pl - 1 - pl : pl);
+    if (j >= (long long)hl * n_qtiles) return false;
+    const int rank = (int)(j / hl);
+    bh = x + hstride * (int)(j - (long long)rank * hl);
     qt = causal ? n_qtiles - 1 - rank : rank;
     return true;
 }
