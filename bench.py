@@ -159,6 +159,9 @@ def main(argv=None):
                          "write MIB) so profiler byte counters can be scaled against it")
     ap.add_argument("--out-dtype", choices=["bf16", "f32"], default=None,
                     help="output storage (default: the input storage type)")
+    ap.add_argument("--layout", choices=["bhnd", "bnhd"], default="bhnd",
+                    help="storage of Q, K, V and O: [B][H][N][d] (default) or [B][N][H][d], "
+                         "the latter passed as strided views (no copies in the timed region)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -189,7 +192,11 @@ def main(argv=None):
         w = synth.WORKLOADS[name]
         host, (tq, tk, tv) = _inputs(w, dev)
         odt = {"bf16": torch.bfloat16, "f32": torch.float32}[args.out_dtype or w.dtype]
-        out = torch.empty((w.B, w.H, w.Nq, w.dv), dtype=odt, device=dev)
+        if args.layout == "bnhd":
+            tq, tk, tv = (t.transpose(1, 2).contiguous().transpose(1, 2) for t in (tq, tk, tv))
+            out = torch.empty((w.B, w.Nq, w.H, w.dv), dtype=odt, device=dev).transpose(1, 2)
+        else:
+            out = torch.empty((w.B, w.H, w.Nq, w.dv), dtype=odt, device=dev)
         ws_bytes = moa.moa_attn_workspace_bytes(w.B, w.H, w.Nq, w.Nk, w.dk, w.dv, 0)
         ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
 
@@ -207,7 +214,8 @@ def main(argv=None):
     if mfma_bound:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                "traffic": measured_traffic("prefill_bf16", w.name) if w.dtype == "bf16" else None}
+                "traffic": measured_traffic("prefill_bf16", w.name)
+                if w.dtype == "bf16" and args.layout == "bhnd" else None}
     else:
         gbs = nbytes / (ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -226,7 +234,7 @@ def main(argv=None):
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "Nq": w.Nq, "Nk": w.Nk, "dk": w.dk,
-                   "dv": w.dv, "causal": w.causal, "in": w.dtype,
+                   "dv": w.dv, "causal": w.causal, "in": w.dtype, "layout": args.layout,
                    "out": args.out_dtype or w.dtype, "flop_per_step": flops,
                    "compulsory_bytes_per_step": nbytes,
                    "hbm_GBps_compulsory": round(nbytes / (ms * 1e-3) / 1e9, 1)},
@@ -245,7 +253,8 @@ def main(argv=None):
             "tflops": round(algorithmic_flops(wd) / (msd * 1e-3) / 1e12, 2),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                         "traffic": measured_traffic("decode_split", wd.name)},
+                         "traffic": measured_traffic("decode_split", wd.name)
+                         if args.layout == "bhnd" else None},
         }
         print(f"# decode {wd.name}: {msd:.4f} ms/call, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
 

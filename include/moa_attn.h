@@ -20,8 +20,9 @@
  * Conventions shared by all entry points
  *  - Plain C types only; no HIP or framework types appear here.  `stream` is a
  *    hipStream_t passed as void* (NULL = the default stream).
- *  - All tensor pointers are DEVICE pointers owned by the caller, contiguous,
- *    row-major (last index fastest; the paper's gamma layout):
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  moa_attn_fwd
+ *    takes contiguous row-major tensors (last index fastest; the paper's gamma
+ *    layout; moa_attn_fwd_strided below takes per-dimension strides):
  *      Q [B][H][Nq][dk]   K [B][H][Nk][dk]   V [B][H][Nk][dv]   O [B][H][Nq][dv]
  *      LSE [B][H][Nq] fp32 (optional, NULL = not written)
  *    Every tensor pointer must be 16-byte aligned.
@@ -122,6 +123,39 @@ int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale, int causal,
                  int in_dtype, int out_dtype, void* workspace, size_t workspace_bytes,
                  int num_splits, void* stream);
+
+/*
+ * moa_attn_fwd_strided -- moa_attn_fwd on strided tensors: the storage
+ * functions of the footnote to eq. gamma with per-dimension strides, i.e.
+ * the Operational Normal Form's offset = base + sum_k stride_k * i_k
+ * (Def. "Operational Normal Form").  Element (b, h, i, e) of Q lives at
+ *   Q + (b*q_strides[0] + h*q_strides[1] + i*q_strides[2] + e) elements,
+ * and likewise for K, V and O; the head dimension e is contiguous.  This
+ * covers the row-major [B][H][N][d] layout, [B][N][H][d] (PyTorch's usual
+ * batch-first layout without a copy), padded rows, packed QKV buffers, and
+ * K/V shared across heads (head stride 0).  A stride array may be NULL, which
+ * means the contiguous row-major strides of moa_attn_fwd.  LSE stays
+ * contiguous [B][H][Nq].  Column-major storage (non-contiguous e) is not
+ * supported by this entry point.
+ *
+ * Stride rules (elements, each array {batch, head, row}):
+ *  - all >= 0 (else MOA_ERR_INVALID_ARG); rows of a tensor with more than one
+ *    row must not overlap (row stride >= d, else MOA_ERR_INVALID_ARG);
+ *  - stride * element size a multiple of 16 bytes, and (rows-1)*row stride + d
+ *    elements within 2^31 bytes per head (else MOA_ERR_UNSUPPORTED);
+ *  - O must not write any element twice (its dimensions of size > 1, ordered
+ *    by stride, must nest without overlap; else MOA_ERR_INVALID_ARG).
+ * Q, K and V may overlap one another (they are only read); O, LSE and the
+ * workspace must not overlap anything, where a strided tensor occupies the
+ * bytes from its base pointer to the end of its last element.
+ * All other arguments, results and status codes are those of moa_attn_fwd.
+ */
+int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                         const int64_t* q_strides, const int64_t* k_strides,
+                         const int64_t* v_strides, const int64_t* o_strides, float scale,
+                         int causal, int in_dtype, int out_dtype, void* workspace,
+                         size_t workspace_bytes, int num_splits, void* stream);
 
 /* moa_attn_status_string -- static, human-readable text for a status code. */
 const char* moa_attn_status_string(int status);

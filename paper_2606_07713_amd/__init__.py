@@ -47,6 +47,9 @@ _i64, _vp, _f32, _ci, _sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, cty
 lib.moa_attn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _f32,
                              _ci, _ci, _ci, _vp, _sz, _ci, _vp]
 lib.moa_attn_fwd.restype = _ci
+lib.moa_attn_fwd_strided.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
+                                     _vp, _vp, _vp, _vp, _f32, _ci, _ci, _ci, _vp, _sz, _ci, _vp]
+lib.moa_attn_fwd_strided.restype = _ci
 lib.moa_attn_workspace_bytes.argtypes = [_i64] * 6 + [_ci]
 lib.moa_attn_workspace_bytes.restype = _sz
 lib.moa_attn_num_splits.argtypes = [_i64] * 6 + [_ci]
@@ -90,6 +93,26 @@ def moa_attn_fwd(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, scale, causal, in_dtype,
                                 stream))
 
 
+def _stride_array(strides):
+    if strides is None:
+        return None
+    if len(strides) != 3:
+        raise ValueError("a stride array has three entries: batch, head, row")
+    return (ctypes.c_int64 * 3)(*[int(x) for x in strides])
+
+
+def moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_strides, v_strides,
+                         o_strides, scale, causal, in_dtype, out_dtype, workspace,
+                         workspace_bytes, num_splits, stream) -> int:
+    """Raw C call with per-tensor (batch, head, row) element strides (3-sequences, or None for
+    the contiguous default); returns the status."""
+    arrs = [_stride_array(x) for x in (q_strides, k_strides, v_strides, o_strides)]
+    ptrs = [ctypes.cast(a, ctypes.c_void_p) if a is not None else None for a in arrs]
+    return int(lib.moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, *ptrs,
+                                        float(scale), int(causal), in_dtype, out_dtype, workspace,
+                                        workspace_bytes, num_splits, stream))
+
+
 def _dtype_code(t):
     import torch
     if t == torch.float32:
@@ -101,10 +124,14 @@ def _dtype_code(t):
 
 def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False,
              num_splits=0, out=None, workspace=None, stream=None):
-    """Fused attention on torch device tensors [B, H, N, d] (contiguous, same dtype).
+    """Fused attention on torch device tensors shaped [B, H, N, d] (same dtype).
 
-    Returns O [B, H, Nq, dv] (and LSE [B, H, Nq] fp32 when ``return_lse``).
-    ``scale`` defaults to 1/sqrt(dk).  Raises ``MoaAttnError`` on a rejected call.
+    The tensors may be any strided views whose last dimension is contiguous (e.g. a
+    [B, N, H, d] tensor viewed with ``.transpose(1, 2)``, or slices of a packed QKV
+    buffer); their strides go to ``moa_attn_fwd_strided`` and nothing is copied.  ``out``
+    may be such a view too.  Returns O [B, H, Nq, dv] (and LSE [B, H, Nq] fp32 when
+    ``return_lse``).  ``scale`` defaults to 1/sqrt(dk).  Raises ``MoaAttnError`` on a
+    rejected call.
     """
     import torch
     if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
@@ -112,8 +139,8 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
     for t in (q, k, v):
         if not t.is_cuda:
             raise ValueError("q, k, v must be device tensors")
-        if not t.is_contiguous():
-            raise ValueError("q, k, v must be contiguous")
+        if t.stride(3) != 1 and t.shape[3] > 1:
+            raise ValueError("the last dimension of q, k, v must be contiguous")
     if not (q.dtype == k.dtype == v.dtype):
         raise TypeError("q, k, v must share one dtype")
     B, H, Nq, dk = q.shape
@@ -127,22 +154,24 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
         scale = 1.0 / math.sqrt(dk)
     if out is None:
         out = torch.empty((B, H, Nq, dv), dtype=odt, device=q.device)
-    elif (tuple(out.shape) != (B, H, Nq, dv) or out.dtype != odt or not out.is_contiguous()
-          or out.device != q.device):
-        raise ValueError("out must be a contiguous [B, H, Nq, dv] tensor of the output dtype")
+    elif (tuple(out.shape) != (B, H, Nq, dv) or out.dtype != odt or out.device != q.device
+          or (out.stride(3) != 1 and dv > 1)):
+        raise ValueError("out must be a [B, H, Nq, dv] tensor of the output dtype whose last "
+                         "dimension is contiguous")
     lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device) if return_lse else None
     ws_bytes = moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    st = moa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                      lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv, scale,
-                      causal, in_code, out_code,
-                      workspace.data_ptr() if workspace is not None else None,
-                      workspace.numel() * workspace.element_size() if workspace is not None else 0,
-                      num_splits,
-                      stream.cuda_stream)
+    st = moa_attn_fwd_strided(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                              lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv,
+                              q.stride()[:3], k.stride()[:3], v.stride()[:3], out.stride()[:3],
+                              scale, causal, in_code, out_code,
+                              workspace.data_ptr() if workspace is not None else None,
+                              workspace.numel() * workspace.element_size()
+                              if workspace is not None else 0,
+                              num_splits, stream.cuda_stream)
     if st != MOA_OK:
         raise MoaAttnError(st)
     return (out, lse) if return_lse else out

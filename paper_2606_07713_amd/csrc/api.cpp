@@ -61,6 +61,50 @@ bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
     return a0 < b0 + bn && b0 < a0 + an;
 }
 
+// Element strides of one tensor over (batch, head, row); d is contiguous.
+struct Strides {
+    int64_t b, h, r;
+};
+
+Strides contiguous(int64_t H, int64_t N, int64_t d) { return {H * N * d, N * d, d}; }
+
+// Checks of one tensor's strides: non-negative, every row 16-byte aligned,
+// rows of d elements that do not overlap, and in-head byte offsets that fit
+// the kernels' 32-bit descriptors.  0 = fine, else a status code.
+int check_strides(const Strides& s, int64_t N, int64_t d, size_t es) {
+    if (s.b < 0 || s.h < 0 || s.r < 0) return MOA_ERR_INVALID_ARG;
+    if (N > 1 && s.r < d) return MOA_ERR_INVALID_ARG;
+    if ((s.b * (int64_t)es) % 16 || (s.h * (int64_t)es) % 16 || (s.r * (int64_t)es) % 16)
+        return MOA_ERR_UNSUPPORTED;
+    const int64_t lim = std::numeric_limits<int32_t>::max();
+    if (s.r > lim / (int64_t)es) return MOA_ERR_UNSUPPORTED;
+    if (N > 0 && ((N - 1) * s.r + d) > lim / (int64_t)es) return MOA_ERR_UNSUPPORTED;
+    return 0;
+}
+
+// Bytes from a tensor's base pointer to the end of its last element.
+size_t extent_bytes(const Strides& s, int64_t B, int64_t H, int64_t N, int64_t d, size_t es) {
+    if (B == 0 || H == 0 || N == 0 || d == 0) return 0;
+    return (size_t)((B - 1) * s.b + (H - 1) * s.h + (N - 1) * s.r + d) * es;
+}
+
+// True if no two (batch, head, row, element) positions share an address:
+// the dimensions of size > 1, by increasing stride, nest without overlap.
+bool injective(const Strides& s, int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (B == 0 || H == 0 || N == 0) return true;   // nothing is written
+    struct Dim { int64_t stride, count; } dims[3] = {{s.b, B}, {s.h, H}, {s.r, N}};
+    for (int i = 0; i < 3; ++i)
+        for (int j = i + 1; j < 3; ++j)
+            if (dims[j].stride < dims[i].stride) { Dim t = dims[i]; dims[i] = dims[j]; dims[j] = t; }
+    int64_t span = d;   // elements covered by the inner dimensions so far
+    for (int i = 0; i < 3; ++i) {
+        if (dims[i].count <= 1) continue;
+        if (dims[i].stride < span) return false;
+        span = dims[i].stride * dims[i].count;
+    }
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -82,10 +126,15 @@ size_t moa_attn_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, in
     return decode_ws_bytes(bh, dk, pick_splits(bh, Nk, num_splits));
 }
 
-int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE, int64_t B,
-                 int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale,
-                 int causal, int in_dtype, int out_dtype, void* workspace,
-                 size_t workspace_bytes, int num_splits, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, int64_t B, int64_t H,
+             int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, const int64_t* q_strides,
+             const int64_t* k_strides, const int64_t* v_strides, const int64_t* o_strides,
+             float scale, int causal, int in_dtype, int out_dtype, void* workspace,
+             size_t workspace_bytes, int num_splits, void* stream) {
     // ---- validation: no HIP call happens before all of it has passed
     if (!Q || !K || !V || !O) return MOA_ERR_INVALID_ARG;
     if (!dims_ok(B, H, Nq, Nk, dk, dv)) return MOA_ERR_INVALID_ARG;
@@ -101,11 +150,25 @@ int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
     if (!head_supported(dk, dv)) return MOA_ERR_UNSUPPORTED;
     if (!sizes_fit(B, H, Nq, Nk, dk)) return MOA_ERR_UNSUPPORTED;
 
-    const int64_t bh = B * H;
     const size_t ies = in_dtype == MOA_F32 ? 4 : 2;
     const size_t oes = out_dtype == MOA_F32 ? 4 : 2;
-    const size_t qn = (size_t)bh * Nq * dk * ies, kn = (size_t)bh * Nk * dk * ies;
-    const size_t vn = (size_t)bh * Nk * dv * ies, on = (size_t)bh * Nq * dv * oes;
+    const Strides sq = q_strides ? Strides{q_strides[0], q_strides[1], q_strides[2]}
+                                 : contiguous(H, Nq, dk);
+    const Strides sk = k_strides ? Strides{k_strides[0], k_strides[1], k_strides[2]}
+                                 : contiguous(H, Nk, dk);
+    const Strides sv = v_strides ? Strides{v_strides[0], v_strides[1], v_strides[2]}
+                                 : contiguous(H, Nk, dv);
+    const Strides so = o_strides ? Strides{o_strides[0], o_strides[1], o_strides[2]}
+                                 : contiguous(H, Nq, dv);
+    int st;
+    if ((st = check_strides(sq, Nq, dk, ies)) || (st = check_strides(sk, Nk, dk, ies)) ||
+        (st = check_strides(sv, Nk, dv, ies)) || (st = check_strides(so, Nq, dv, oes)))
+        return st;
+    if (!injective(so, B, H, Nq, dv)) return MOA_ERR_INVALID_ARG;
+
+    const int64_t bh = B * H;
+    const size_t qn = extent_bytes(sq, B, H, Nq, dk, ies), kn = extent_bytes(sk, B, H, Nk, dk, ies);
+    const size_t vn = extent_bytes(sv, B, H, Nk, dv, ies), on = extent_bytes(so, B, H, Nq, dv, oes);
     const size_t ln = LSE ? (size_t)bh * Nq * sizeof(float) : 0;
     if (overlaps(O, on, Q, qn) || overlaps(O, on, K, kn) || overlaps(O, on, V, vn))
         return MOA_ERR_INVALID_ARG;
@@ -135,6 +198,11 @@ int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
     p.causal = causal != 0;
     p.in_bf16 = in_dtype == MOA_BF16;
     p.out_bf16 = out_dtype == MOA_BF16;
+    p.lay.qb = sq.b; p.lay.qh = sq.h; p.lay.qr = (int)sq.r;
+    p.lay.kb = sk.b; p.lay.kh = sk.h; p.lay.kr = (int)sk.r;
+    p.lay.vb = sv.b; p.lay.vh = sv.h; p.lay.vr = (int)sv.r;
+    p.lay.ob = so.b; p.lay.oh = so.h; p.lay.orow = (int)so.r;
+    p.lay.H = (int)H;
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     hipError_t e;
@@ -149,6 +217,30 @@ int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
         return MOA_ERR_HIP;
     }
     return MOA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE, int64_t B,
+                 int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, float scale,
+                 int causal, int in_dtype, int out_dtype, void* workspace,
+                 size_t workspace_bytes, int num_splits, void* stream) {
+    return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, nullptr, nullptr, nullptr, nullptr,
+                    scale, causal, in_dtype, out_dtype, workspace, workspace_bytes, num_splits,
+                    stream);
+}
+
+int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                         const int64_t* q_strides, const int64_t* k_strides,
+                         const int64_t* v_strides, const int64_t* o_strides, float scale,
+                         int causal, int in_dtype, int out_dtype, void* workspace,
+                         size_t workspace_bytes, int num_splits, void* stream) {
+    return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_strides, v_strides,
+                    o_strides, scale, causal, in_dtype, out_dtype, workspace, workspace_bytes,
+                    num_splits, stream);
 }
 
 const char* moa_attn_last_hip_error(void) { return g_last_hip_error; }

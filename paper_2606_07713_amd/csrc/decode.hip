@@ -69,7 +69,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(THREADS) void decode_split_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int Nk, int splits,
-    int keys_per_split, float c) {
+    int keys_per_split, float c, Layout L) {
     using C = Cfg<T, D>;
     constexpr int EPL = C::EPL, LPR = C::LPR, RPW = C::RPW, STEP = C::STEP;
     __shared__ float red_m[WAVES], red_l[WAVES];
@@ -83,10 +83,10 @@ __global__ __launch_bounds__(THREADS) void decode_split_kernel(
     const int k_begin = sp * keys_per_split;
     const int k_end = min(Nk, k_begin + keys_per_split);
 
-    const T* Kh = K + (size_t)bh * Nk * D;
-    const T* Vh = V + (size_t)bh * Nk * D;
+    const T* Kh = K + head_offset(bh, L.H, L.kb, L.kh);
+    const T* Vh = V + head_offset(bh, L.H, L.vb, L.vh);
     float qv[EPL];
-    widen<T>(*reinterpret_cast<const uint4*>(Q + (size_t)bh * D + el * EPL), qv);
+    widen<T>(*reinterpret_cast<const uint4*>(Q + head_offset(bh, L.H, L.qb, L.qh) + el * EPL), qv);
 
     float m = kNegInf, l = 0.0f, acc[EPL];
 #pragma unroll
@@ -97,12 +97,12 @@ __global__ __launch_bounds__(THREADS) void decode_split_kernel(
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int key = min(kb + u * RPW + grp, k_end - 1);
-            kr[u] = load_nt16(Kh + (size_t)key * D + el * EPL);
+            kr[u] = load_nt16(Kh + (size_t)key * L.kr + el * EPL);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int key = min(kb + u * RPW + grp, k_end - 1);
-            vr[u] = load_nt16(Vh + (size_t)key * D + el * EPL);
+            vr[u] = load_nt16(Vh + (size_t)key * L.vr + el * EPL);
         }
         // scores (log2 units) of the U keys this lane group holds
         float t[U];
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(THREADS) void decode_split_kernel(
 template <int D, bool OUT_BF16>
 __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ ws_acc, const float* __restrict__ ws_ml, void* __restrict__ Out,
-    float* __restrict__ LSE, int splits) {
+    float* __restrict__ LSE, int splits, Layout lay) {
     constexpr int PER = D / 64;
     const int bh = blockIdx.x;
     const int lane = threadIdx.x;
@@ -197,7 +197,7 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float inv = 1.0f / L;
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-        const size_t idx = (size_t)bh * D + e * 64 + lane;
+        const size_t idx = (size_t)head_offset(bh, lay.H, lay.ob, lay.oh) + e * 64 + lane;
         if (OUT_BF16)
             static_cast<u16*>(Out)[idx] = (u16)f32_to_bf16_bits(o[e] * inv);
         else
@@ -215,15 +215,15 @@ hipError_t launch_t(const Problem& p, int splits, float* ws, hipStream_t stream)
     hipError_t e = launch_kernel(decode_split_kernel<T, D>, dim3((unsigned)blocks), dim3(THREADS),
                                  stream, static_cast<const T*>(p.q), static_cast<const T*>(p.k),
                                  static_cast<const T*>(p.v), ws_acc, ws_ml, p.nk, splits, kps,
-                                 p.scale * kLog2e);
+                                 p.scale * kLog2e, p.lay);
     if (e != hipSuccess) return e;
     if (p.out_bf16)
         return launch_kernel(decode_combine_kernel<D, true>, dim3(p.bh), dim3(64), stream,
                              static_cast<const float*>(ws_acc), static_cast<const float*>(ws_ml),
-                             p.o, p.lse, splits);
+                             p.o, p.lse, splits, p.lay);
     return launch_kernel(decode_combine_kernel<D, false>, dim3(p.bh), dim3(64), stream,
                          static_cast<const float*>(ws_acc), static_cast<const float*>(ws_ml), p.o,
-                         p.lse, splits);
+                         p.lse, splits, p.lay);
 }
 
 }  // namespace

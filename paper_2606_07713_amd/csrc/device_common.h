@@ -81,6 +81,19 @@ inline hipError_t launch_kernel(void (*kernel)(Params...), dim3 grid, dim3 block
     return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, 0, stream);
 }
 
+// Element offset of the (batch*head) slice bh of a tensor with batch stride
+// sb and head stride sh, H heads.
+__device__ __forceinline__ long long head_offset(int bh, int H, long long sb, long long sh) {
+    const int b = bh / H;
+    return (long long)b * sb + (long long)(bh - b * H) * sh;
+}
+
+// Bytes spanned by n rows of row_bytes each, row_stride_bytes apart (the
+// extent a buffer descriptor over those rows must cover).
+__device__ __forceinline__ uint32_t rows_extent(int n, uint32_t row_stride_bytes, uint32_t row_bytes) {
+    return n > 0 ? (uint32_t)(n - 1) * row_stride_bytes + row_bytes : 0u;
+}
+
 // Raw buffer access: a descriptor over [base, base + bytes).  Loads beyond
 // `bytes` return zeros instead of touching memory, which is how ragged tiles
 // are padded without per-lane clamping.  (Descriptor word 3 for gfx9-family.)

@@ -7,6 +7,15 @@
 
 namespace moa {
 
+// Element strides of Q, K, V and O over batch and head (64-bit) and over
+// rows (32-bit); the d dimension of every tensor is contiguous.  Contiguous
+// [B][H][N][d] tensors have (batch, head, row) strides (H*N*d, N*d, d).
+struct Layout {
+    long long qb, qh, kb, kh, vb, vh, ob, oh;
+    int qr, kr, vr, orow;
+    int H;             // heads, to split a (batch*head) index
+};
+
 // One fused-attention problem after validation.  Pointers are device
 // pointers; sizes are already checked to fit the kernels' 32-bit in-head
 // offsets.
@@ -22,7 +31,17 @@ struct Problem {
     bool causal;
     bool in_bf16;
     bool out_bf16;
+    Layout lay;
 };
+
+// True if every tensor of `p` has the contiguous [B][H][N][d] strides.
+inline bool is_contiguous(const Problem& p) {
+    const Layout& L = p.lay;
+    const long long d = p.d, nq = p.nq, nk = p.nk, H = L.H;
+    return L.qr == d && L.qh == nq * d && L.qb == H * nq * d && L.kr == d && L.kh == nk * d &&
+           L.kb == H * nk * d && L.vr == d && L.vh == nk * d && L.vb == H * nk * d &&
+           L.orow == d && L.oh == nq * d && L.ob == H * nq * d;
+}
 
 // Prefill, bf16 inputs: one launch of the MFMA tile kernel.
 hipError_t launch_prefill_bf16(const Problem& p, hipStream_t stream);

@@ -63,10 +63,12 @@ __device__ __forceinline__ void wait_loads_to_lds() {
 //   groups in the same phase), and group 1 hands its softmax state (m, l, O)
 //   to group 0 through LDS at the end for an exact merge.  Used when the
 //   ping-pong grid is too small to fill the GPU.
-template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT>
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED>
 __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
-    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c) {
+    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c,
+    Layout L) {
+    const Addr<D, STRIDED> A{L, Nq, Nk};
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
     constexpr int NG = KSPLIT ? 2 : 1;                    // independent key streams
@@ -114,19 +116,20 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     if (!item_of(blockIdx.x, item, gridDim.x, n_bh, n_qtiles, CAUSAL, bh, qt)) break;
     const int q0 = qt * BMQ;
 
-    const u16* Qh = Q + (size_t)bh * Nq * D;
-    const u16* Kh = K + (size_t)bh * Nk * D;
-    const u16* Vh = V + (size_t)bh * Nk * D;
+    const u16* Qh = Q + A.q_head(bh);
+    const u16* Kh = K + A.k_head(bh);
+    const u16* Vh = V + A.v_head(bh);
 
     // ---- a1: Q fragment for this lane's query, all of d, kept in registers.
     // Rows past Nq read as zeros (buffer bounds) and are never stored.
     const int qrow = q0 + qw * 32 + col;
     bf16x8 qf[D / 16];
     {
-        const auto rq = make_rsrc(Qh, (uint32_t)Nq * RB);
+        const uint32_t qrb = (uint32_t)A.qr() * 2u;
+        const auto rq = make_rsrc(Qh, rows_extent(Nq, qrb, RB));
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) {
-            uint4 w = buffer_load16(rq, (uint32_t)qrow * RB + s * 32 + half * 16);
+            uint4 w = buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16);
             w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
             qf[s] = __builtin_bit_cast(bf16x8, w);
         }
@@ -148,20 +151,27 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // ---- a2: direct-to-LDS tile loads.  Lane l of the i-th load of loader lw
     // fills slot S = (lw*LPW + i)*64 + l of its stream's tile, which holds
     // logical chunk (S % CHUNKS) ^ swz(row) of row S / CHUNKS.
-    uint32_t ld_voff[LPW];
+    // The global offsets follow each tensor's row stride (kr, vr elements).
+    const uint32_t krb = (uint32_t)A.kr() * 2u, vrb = (uint32_t)A.vr() * 2u;
+    uint32_t ld_koff[LPW], ld_voff[LPW];
 #pragma unroll
     for (int i = 0; i < LPW; ++i) {
         const int slot = (lw * LPW + i) * 64 + lane;
         const int row = slot / C::CHUNKS, p = slot % C::CHUNKS;
-        ld_voff[i] = (uint32_t)row * RB + (uint32_t)((p ^ swz<D>(row)) * 16);
+        const uint32_t chunk = (uint32_t)((p ^ swz<D>(row)) * 16);
+        ld_koff[i] = (uint32_t)row * krb + chunk;
+        ld_voff[i] = (uint32_t)row * vrb + chunk;
     }
-    // Loads the stream's local tile t into `stage` (only while t < g_count).
-    auto issue_tile_load = [&](const u16* head, int t, unsigned char* stage) {
+    // Loads the stream's local tile t of K or V into `stage` (only while
+    // t < g_count).
+    auto issue_tile_load = [&](bool is_k, int t, unsigned char* stage) {
         const int kbase = (g_start + t) * BN;
-        const auto r = make_rsrc(head + (size_t)kbase * D, (uint32_t)(Nk - kbase) * RB);
+        const u16* head = is_k ? Kh : Vh;
+        const int rs = is_k ? A.kr() : A.vr();
+        const auto r = make_rsrc(head + (size_t)kbase * rs, rows_extent(Nk - kbase, (uint32_t)rs * 2u, RB));
 #pragma unroll
         for (int i = 0; i < LPW; ++i)
-            buffer_load16_to_lds(r, stage + g_off + (lw * LPW + i) * 1024, ld_voff[i]);
+            buffer_load16_to_lds(r, stage + g_off + (lw * LPW + i) * 1024, is_k ? ld_koff[i] : ld_voff[i]);
     };
 
     // Per-lane LDS addresses of the MFMA operand reads (stage, key block and
@@ -347,13 +357,13 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // guards no LDS data, so it carries no memory fence (which would wait for
     // the loads in flight at mid-slot).
     const bool lead = KSPLIT || grp == 0;
-    if (g_count > 0) issue_tile_load(Kh, 0, k_st0);
+    if (g_count > 0) issue_tile_load(true, 0, k_st0);
     wait_loads_to_lds();
     __syncthreads();
     for (int t = 0; t <= n_iter; t += 2) {
         // ---- even tile t (parity 0)
-        if (t + 1 < g_count) issue_tile_load(Kh, t + 1, k_st1);
-        if (t < g_count) issue_tile_load(Vh, t, v_st0);
+        if (t + 1 < g_count) issue_tile_load(true, t + 1, k_st1);
+        if (t < g_count) issue_tile_load(false, t, v_st0);
         if (lead) gemm_phase(t, S0{});
         else if (t >= 1) softmax_phase(t - 1);
         if constexpr (!KSPLIT) barrier_no_fence();
@@ -363,8 +373,8 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         __syncthreads();
         if (t + 1 > n_iter) break;
         // ---- odd tile t + 1 (parity 1)
-        if (t + 2 < g_count) issue_tile_load(Kh, t + 2, k_st0);
-        if (t + 1 < g_count) issue_tile_load(Vh, t + 1, v_st1);
+        if (t + 2 < g_count) issue_tile_load(true, t + 2, k_st0);
+        if (t + 1 < g_count) issue_tile_load(false, t + 1, v_st1);
         if (lead) gemm_phase(t + 1, S1{});
         else softmax_phase(t);
         if constexpr (!KSPLIT) barrier_no_fence();
@@ -410,7 +420,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
     if (qrow < Nq) {
-        const size_t obase = ((size_t)bh * Nq + qrow) * D;
+        const size_t obase = (size_t)A.o_head(bh) + (size_t)qrow * A.orow();
 #pragma unroll
         for (int b = 0; b < D / 32; ++b) {
 #pragma unroll
@@ -445,9 +455,9 @@ constexpr long long kPingPongFromItems = 1024;
 
 // One persistent launch: as many workgroups as the device holds at once, at
 // most one per work item.
-template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT>
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED>
 hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, hipStream_t stream) {
-    auto kernel = prefill_bf16_kernel<D, CAUSAL, OUT_BF16, KSPLIT>;
+    auto kernel = prefill_bf16_kernel<D, CAUSAL, OUT_BF16, KSPLIT, STRIDED>;
     static const int per_cu = [&] {
         int n = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, THREADS, 0) != hipSuccess) n = 1;
@@ -460,29 +470,37 @@ hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, hipStream_
     const unsigned grid = (unsigned)std::min<long long>(items, (long long)cus * per_cu);
     return launch_kernel(kernel, dim3(grid), dim3(THREADS), stream,
                          static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
-                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, p.bh, n_qtiles, c);
+                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, p.bh, n_qtiles, c,
+                         p.lay);
 }
 
-template <int D, bool CAUSAL, bool OUT_BF16>
+template <int D, bool CAUSAL, bool OUT_BF16, bool STRIDED>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const float c = p.scale * kLog2e;
     const int qt_pp = (p.nq + BM - 1) / BM;
     const long long items = (long long)p.bh * qt_pp;
     if (items >= kPingPongFromItems || p.nk <= BN)
-        return launch_persistent<D, CAUSAL, OUT_BF16, false>(p, qt_pp, c, stream);
+        return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, stream);
     int cus = 0;
     const hipError_t e = device_cus(stream, cus);
     if (e != hipSuccess) return e;
     if (items >= cus) return launch_prefill_bf16_pipe(p, stream);
     const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
-    return launch_persistent<D, CAUSAL, OUT_BF16, true>(p, qt_ks, c, stream);
+    return launch_persistent<D, CAUSAL, OUT_BF16, true, STRIDED>(p, qt_ks, c, stream);
+}
+
+template <int D, bool STRIDED>
+hipError_t launch_s(const Problem& p, hipStream_t stream) {
+    if (p.causal)
+        return p.out_bf16 ? launch<D, true, true, STRIDED>(p, stream)
+                          : launch<D, true, false, STRIDED>(p, stream);
+    return p.out_bf16 ? launch<D, false, true, STRIDED>(p, stream)
+                      : launch<D, false, false, STRIDED>(p, stream);
 }
 
 template <int D>
 hipError_t launch_d(const Problem& p, hipStream_t stream) {
-    if (p.causal)
-        return p.out_bf16 ? launch<D, true, true>(p, stream) : launch<D, true, false>(p, stream);
-    return p.out_bf16 ? launch<D, false, true>(p, stream) : launch<D, false, false>(p, stream);
+    return is_contiguous(p) ? launch_s<D, false>(p, stream) : launch_s<D, true>(p, stream);
 }
 
 }  // namespace

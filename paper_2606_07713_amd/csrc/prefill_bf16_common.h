@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "device_common.h"
+#include "launch.h"
 
 namespace moa {
 namespace pf {
@@ -79,6 +80,36 @@ __device__ __forceinline__ bool item_of(int p, int i, int P, int n_bh, int n_qti
     qt = causal ? n_qtiles - 1 - rank : rank;
     return true;
 }
+
+// Element offsets as the kernels use them: the general strided Layout, or
+// (STRIDED = false) the contiguous [B][H][N][d] layout with compile-time row
+// strides, which keeps the stride arithmetic out of the registers of the
+// common case.
+template <int D, bool STRIDED>
+struct Addr {
+    const Layout& L;
+    int Nq, Nk;
+    __device__ __forceinline__ long long q_head(int bh) const {
+        if constexpr (STRIDED) return head_offset(bh, L.H, L.qb, L.qh);
+        return (long long)bh * Nq * D;
+    }
+    __device__ __forceinline__ long long k_head(int bh) const {
+        if constexpr (STRIDED) return head_offset(bh, L.H, L.kb, L.kh);
+        return (long long)bh * Nk * D;
+    }
+    __device__ __forceinline__ long long v_head(int bh) const {
+        if constexpr (STRIDED) return head_offset(bh, L.H, L.vb, L.vh);
+        return (long long)bh * Nk * D;
+    }
+    __device__ __forceinline__ long long o_head(int bh) const {
+        if constexpr (STRIDED) return head_offset(bh, L.H, L.ob, L.oh);
+        return (long long)bh * Nq * D;
+    }
+    __device__ __forceinline__ int qr() const { if constexpr (STRIDED) return L.qr; return D; }
+    __device__ __forceinline__ int kr() const { if constexpr (STRIDED) return L.kr; return D; }
+    __device__ __forceinline__ int vr() const { if constexpr (STRIDED) return L.vr; return D; }
+    __device__ __forceinline__ int orow() const { if constexpr (STRIDED) return L.orow; return D; }
+};
 
 // s_waitcnt with vmcnt(N) and the other counters left alone (gfx9 encoding:
 // vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).

@@ -53,10 +53,12 @@ constexpr int RING = 2;          // LDS stages per K ring and per V ring
 template <int N>
 using Tag = std::integral_constant<int, N>;
 
-template <int D, bool CAUSAL, bool OUT_BF16>
+template <int D, bool CAUSAL, bool OUT_BF16, bool STRIDED>
 __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
-    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c) {
+    void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c,
+    Layout L) {
+    const Addr<D, STRIDED> A{L, Nq, Nk};
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
     constexpr int LPS = C::TILE_BYTES / (WAVES * 1024);   // 16-byte loads per lane per stage
@@ -92,12 +94,16 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
     // S = (w*LPS + i)*64 + l of the stage (contiguous across the workgroup)
     // and stores it at LDS row S / CHUNKS, physical chunk (S % CHUNKS) ^
     // swz(row).
-    uint32_t st_woff[LPS];
+    // The global offsets follow each tensor's row stride (kr, vr elements).
+    const uint32_t krb = (uint32_t)A.kr() * 2u, vrb = (uint32_t)A.vr() * 2u;
+    uint32_t st_woff[LPS], st_koff[LPS], st_voff[LPS];
 #pragma unroll
     for (int i = 0; i < LPS; ++i) {
         const int slot = (wave * LPS + i) * 64 + lane;
         const int row = slot / C::CHUNKS, p = slot % C::CHUNKS;
         st_woff[i] = (uint32_t)row * RB + (uint32_t)((p ^ swz<D>(row)) * 16);
+        st_koff[i] = (uint32_t)row * krb + (uint32_t)(p * 16);
+        st_voff[i] = (uint32_t)row * vrb + (uint32_t)(p * 16);
     }
     // Per-lane LDS addresses of the MFMA operand reads; the 32-key half of a
     // stage and the 16-key chunk are added as immediates.
@@ -123,19 +129,20 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
         int bh, qt;
         if (!item_of(blockIdx.x, item, gridDim.x, n_bh, n_qtiles, CAUSAL, bh, qt)) break;
         const int q0 = qt * BMQ;
-        const u16* Qh = Q + (size_t)bh * Nq * D;
-        const u16* Kh = K + (size_t)bh * Nk * D;
-        const u16* Vh = V + (size_t)bh * Nk * D;
+        const u16* Qh = Q + A.q_head(bh);
+        const u16* Kh = K + A.k_head(bh);
+        const u16* Vh = V + A.v_head(bh);
 
         // ---- a1: Q fragment for this lane's query, all of d, in registers.
         // Rows past Nq read as zeros (buffer bounds) and are never stored.
         const int qrow = q0 + wave * 32 + col;
         bf16x8 qf[D / 16];
         {
-            const auto rq = make_rsrc(Qh, (uint32_t)Nq * RB);
+            const uint32_t qrb = (uint32_t)A.qr() * 2u;
+            const auto rq = make_rsrc(Qh, rows_extent(Nq, qrb, RB));
 #pragma unroll
             for (int s = 0; s < D / 16; ++s) {
-                uint4 w = buffer_load16(rq, (uint32_t)qrow * RB + s * 32 + half * 16);
+                uint4 w = buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16);
                 w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
                 qf[s] = __builtin_bit_cast(bf16x8, w);
             }
@@ -153,12 +160,13 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
         // ---- a2: stage j (keys 64j .. 64j + 63) of K or V: this lane's
         // share into registers (rows past Nk read as zeros), then into an LDS
         // slot one stage iteration later.
-        auto load_stage = [&](const u16* head, int j, uint4 (&st)[LPS]) __attribute__((always_inline)) {
+        auto load_stage = [&](bool is_k, int j, uint4 (&st)[LPS]) __attribute__((always_inline)) {
             const int kb = min(j * BN, Nk);
-            const auto r = make_rsrc(head + (size_t)kb * D, (uint32_t)(Nk - kb) * RB);
+            const u16* head = is_k ? Kh : Vh;
+            const int rs = is_k ? A.kr() : A.vr();
+            const auto r = make_rsrc(head + (size_t)kb * rs, rows_extent(Nk - kb, (uint32_t)rs * 2u, RB));
 #pragma unroll
-            for (int i = 0; i < LPS; ++i)
-                st[i] = buffer_load16(r, (uint32_t)(((wave * LPS + i) * 64 + lane) * 16));
+            for (int i = 0; i < LPS; ++i) st[i] = buffer_load16(r, is_k ? st_koff[i] : st_voff[i]);
         };
         auto store_stage = [&](unsigned char* slot, const uint4 (&st)[LPS]) __attribute__((always_inline)) {
 #pragma unroll
@@ -395,8 +403,8 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
             barrier_no_fence();
             store_stage(kslot(Tag<S>{}), stK);
             store_stage(vslot(Tag<S + 1>{}), stV);
-            load_stage(Kh, i + 3, stK);
-            load_stage(Vh, i + 2, stV);
+            load_stage(true, i + 3, stK);
+            load_stage(false, i + 2, stV);
             const unsigned char* ks = kslot(Tag<S + 1>{});
             const unsigned char* vs = vslot(Tag<S>{});
             const int t1 = 2 * i + 1, t2 = 2 * i + 2;
@@ -410,15 +418,15 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
         // then S(0) and step 0 from K stage 0.
         {
             uint4 k1[LPS];
-            load_stage(Kh, 0, stK);
-            load_stage(Vh, 0, stV);
-            load_stage(Kh, 1, k1);
+            load_stage(true, 0, stK);
+            load_stage(false, 0, stV);
+            load_stage(true, 1, k1);
             store_stage(k_r0, stK);
             store_stage(v_r0, stV);
             store_stage(k_r1, k1);
         }
-        load_stage(Kh, 2, stK);
-        load_stage(Vh, 1, stV);
+        load_stage(true, 2, stK);
+        load_stage(false, 1, stV);
         wait_lgkmcnt0();
         barrier_no_fence();
         if (n_w > 0) s_mfma(k_r0, 0, sA);
@@ -436,7 +444,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
         const float l_tot = half_sum(l_run);
         const float inv = 1.0f / l_tot;
         if (qrow < Nq) {
-            const size_t obase = ((size_t)bh * Nq + qrow) * D;
+            const size_t obase = (size_t)A.o_head(bh) + (size_t)qrow * A.orow();
 #pragma unroll
             for (int b = 0; b < D / 32; ++b) {
 #pragma unroll
@@ -459,9 +467,9 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
     }
 }
 
-template <int D, bool CAUSAL, bool OUT_BF16>
+template <int D, bool CAUSAL, bool OUT_BF16, bool STRIDED>
 hipError_t launch(const Problem& p, hipStream_t stream) {
-    auto kernel = prefill_pipe_kernel<D, CAUSAL, OUT_BF16>;
+    auto kernel = prefill_pipe_kernel<D, CAUSAL, OUT_BF16, STRIDED>;
     static const int per_cu = [&] {
         int n = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, THREADS, 0) != hipSuccess) n = 1;
@@ -476,14 +484,21 @@ hipError_t launch(const Problem& p, hipStream_t stream) {
     return launch_kernel(kernel, dim3(grid), dim3(THREADS), stream,
                          static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
                          static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, p.bh, n_qtiles,
-                         p.scale * kLog2e);
+                         p.scale * kLog2e, p.lay);
+}
+
+template <int D, bool STRIDED>
+hipError_t launch_s(const Problem& p, hipStream_t stream) {
+    if (p.causal)
+        return p.out_bf16 ? launch<D, true, true, STRIDED>(p, stream)
+                          : launch<D, true, false, STRIDED>(p, stream);
+    return p.out_bf16 ? launch<D, false, true, STRIDED>(p, stream)
+                      : launch<D, false, false, STRIDED>(p, stream);
 }
 
 template <int D>
 hipError_t launch_d(const Problem& p, hipStream_t stream) {
-    if (p.causal)
-        return p.out_bf16 ? launch<D, true, true>(p, stream) : launch<D, true, false>(p, stream);
-    return p.out_bf16 ? launch<D, false, true>(p, stream) : launch<D, false, false>(p, stream);
+    return is_contiguous(p) ? launch_s<D, false>(p, stream) : launch_s<D, true>(p, stream);
 }
 
 }  // namespace

@@ -21,7 +21,8 @@ constexpr int KT = 32;            // keys per tile
 template <int D, bool CAUSAL>
 __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
-    float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c) {
+    float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c,
+    Layout L) {
     constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
     __shared__ __attribute__((aligned(16))) float Ks[KT * D];
     __shared__ __attribute__((aligned(16))) float Vs[KT * D];
@@ -34,14 +35,14 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
     const int qrow_c = qrow < Nq ? qrow : Nq - 1;
     const int off = Nk - Nq;
 
-    const float* Qh = Q + (size_t)bh * Nq * D;
-    const float* Kh = K + (size_t)bh * Nk * D;
-    const float* Vh = V + (size_t)bh * Nk * D;
+    const float* Qh = Q + head_offset(bh, L.H, L.qb, L.qh);
+    const float* Kh = K + head_offset(bh, L.H, L.kb, L.kh);
+    const float* Vh = V + head_offset(bh, L.H, L.vb, L.vh);
 
     float4 qv[CH], acc[CH];
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
-        qv[j] = *reinterpret_cast<const float4*>(Qh + (size_t)qrow_c * D + (j * 4 + quad) * 4);
+        qv[j] = *reinterpret_cast<const float4*>(Qh + (size_t)qrow_c * L.qr + (j * 4 + quad) * 4);
         acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     float m_run = kNegInf, l_run = 0.0f;
@@ -57,9 +58,9 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
             const int row = idx / (D / 4), ch = idx % (D / 4);
             const int key = min(kbase + row, Nk - 1);
             *reinterpret_cast<float4*>(&Ks[row * D + ch * 4]) =
-                *reinterpret_cast<const float4*>(Kh + (size_t)key * D + ch * 4);
+                *reinterpret_cast<const float4*>(Kh + (size_t)key * L.kr + ch * 4);
             *reinterpret_cast<float4*>(&Vs[row * D + ch * 4]) =
-                *reinterpret_cast<const float4*>(Vh + (size_t)key * D + ch * 4);
+                *reinterpret_cast<const float4*>(Vh + (size_t)key * L.vr + ch * 4);
         }
         __syncthreads();
 
@@ -110,7 +111,7 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
 
     if (qrow < Nq) {
         const float inv = 1.0f / l_run;
-        const size_t obase = ((size_t)bh * Nq + qrow) * D;
+        const size_t obase = (size_t)head_offset(bh, L.H, L.ob, L.oh) + (size_t)qrow * L.orow;
 #pragma unroll
         for (int h = 0; h < CH; ++h) {
             const int d0 = (h * 4 + quad) * 4;
@@ -129,7 +130,7 @@ hipError_t launch(const Problem& p, hipStream_t stream) {
     return launch_kernel(prefill_f32_kernel<D, CAUSAL>, dim3((unsigned)blocks), dim3(THREADS),
                          stream, static_cast<const float*>(p.q), static_cast<const float*>(p.k),
                          static_cast<const float*>(p.v), static_cast<float*>(p.o), p.lse, p.nq,
-                         p.nk, n_qtiles, p.scale * kLog2e);
+                         p.nk, n_qtiles, p.scale * kLog2e, p.lay);
 }
 
 template <int D>

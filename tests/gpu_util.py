@@ -46,6 +46,7 @@ def sample_rows(B, H, Nq, n, seed=0, tile=128):
     """Flat rows (b*H + h)*Nq + i: tile edges of the first/last heads plus random rows."""
     rng = np.random.default_rng(seed)
     total = B * H * Nq
+    n = min(n, total)
     edges = {min(i, Nq - 1) for i in (0, 1, Nq - 1, tile - 1, tile, Nq // 2)}
     rows = set()
     for bh in {0, B * H - 1, (B * H) // 2}:

@@ -20,8 +20,8 @@ def _declared_functions():
 
 def test_header_declares_the_entry_points():
     names = _declared_functions()
-    assert names == ["moa_attn_fwd", "moa_attn_last_hip_error", "moa_attn_num_splits",
-                     "moa_attn_status_string", "moa_attn_workspace_bytes"]
+    assert names == ["moa_attn_fwd", "moa_attn_fwd_strided", "moa_attn_last_hip_error",
+                     "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_workspace_bytes"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -98,6 +98,47 @@ def _call(**kw):
 ])
 def test_validation_rejects_before_any_gpu_work(kw, status):
     assert _call(**kw) == status
+
+
+def _call_strided(**kw):
+    args = dict(Q=A, K=BUF, V=C, O=D, LSE=None, B=2, H=4, Nq=8, Nk=8, dk=64, dv=64,
+                q_strides=None, k_strides=None, v_strides=None, o_strides=None, scale=0.125,
+                causal=0, in_dtype=moa.MOA_BF16, out_dtype=moa.MOA_BF16, workspace=None,
+                workspace_bytes=0, num_splits=0, stream=None)
+    args.update(kw)
+    return moa.moa_attn_fwd_strided(**args)
+
+
+# [B, N, H, d] storage of a [B, H, N, d] view: (batch, head, row) strides.
+BSHD = (8 * 4 * 64, 64, 4 * 64)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q_strides=(-1, 64, 64)), 1),                 # negative stride
+    (dict(k_strides=(4096, 512, 32)), 1),              # rows of K overlap (row stride < d)
+    (dict(o_strides=(512, 0, 64)), 1),                 # O heads write the same rows
+    (dict(o_strides=(64, 512, 64)), 1),                # O batches collide with rows
+    (dict(q_strides=(4096, 512, 68)), 2),              # rows not 16-byte aligned (bf16)
+    (dict(v_strides=(4096, 512, 1 << 28)), 2),         # in-head offsets beyond 2^31 bytes
+    (dict(in_dtype=0, out_dtype=0, q_strides=(4096, 512, 66)), 2),   # fp32 rows misaligned
+    (dict(O=A + 4096, q_strides=BSHD), 1),             # O inside Q's strided extent
+    (dict(Q=None), 1), (dict(dk=96, dv=96), 2),        # the usual checks still apply
+])
+def test_strided_validation_rejects_before_any_gpu_work(kw, status):
+    assert _call_strided(**kw) == status
+
+
+def test_strided_accepts_common_layouts_without_gpu_work():
+    # Empty batches are no-ops after validation: valid layouts return OK
+    # without touching the (fake) addresses.
+    for layout in (None, BSHD):
+        assert _call_strided(B=0, q_strides=layout, k_strides=layout, v_strides=layout,
+                             o_strides=layout) == moa.MOA_OK
+    # K/V shared by all heads (head stride 0) and a padded row stride are valid.
+    assert _call_strided(Nq=0, k_strides=(8 * 64, 0, 64), v_strides=(8 * 64, 0, 64),
+                         q_strides=(4 * 8 * 72, 8 * 72, 72)) == moa.MOA_OK
+    # A NULL stride array means the contiguous layout of moa_attn_fwd.
+    assert _call_strided(B=0) == _call(B=0) == moa.MOA_OK
 
 
 def test_empty_problems_are_no_ops():
