@@ -51,7 +51,9 @@ def _load():
         lib.oracle_attn_fwd.argtypes = [vp, vp, vp, ci] + dims + [f32, ci, vp, vp, ci]
         lib.oracle_attn_rows.argtypes = [vp, vp, vp, ci] + dims + [f32, ci, vp, i64, vp, vp, ci]
         lib.oracle_attn_weights.argtypes = [vp, vp, vp, ci] + dims + [f32, ci, vp, vp, vp, vp]
-        for f in (lib.oracle_attn_fwd, lib.oracle_attn_rows, lib.oracle_attn_weights):
+        lib.oracle_attn_bwd.argtypes = [vp, vp, vp, vp, ci] + dims + [f32, ci, vp, vp, vp, ci]
+        for f in (lib.oracle_attn_fwd, lib.oracle_attn_rows, lib.oracle_attn_weights,
+                  lib.oracle_attn_bwd):
             f.restype = ci
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ci
@@ -125,6 +127,24 @@ def attention_weights(q, k, v, scale=None, causal=False):
     if rc != 0:
         raise ValueError(f"oracle_attn_weights rejected the problem (code {rc})")
     return s, p, o, lse
+
+
+def attention_bwd(q, k, v, do, scale=None, causal=False, nthreads=0):
+    """Gradients (dQ, dK, dV), fp64, of a loss whose gradient through O is ``do``
+    ([B,H,Nq,dv], same storage type as q, k, v)."""
+    q, k, v, dt, (B, H, Nq, Nk, dk, dv) = _prep(q, k, v)
+    do = np.ascontiguousarray(do)
+    if do.dtype != q.dtype or do.shape != (B, H, Nq, dv):
+        raise ValueError("dO must have the storage type of Q and shape [B, H, Nq, dv]")
+    dq = np.empty((B, H, Nq, dk), dtype=np.float64)
+    dk_ = np.empty((B, H, Nk, dk), dtype=np.float64)
+    dv_ = np.empty((B, H, Nk, dv), dtype=np.float64)
+    rc = _load().oracle_attn_bwd(q.ctypes.data, k.ctypes.data, v.ctypes.data, do.ctypes.data, dt,
+                                 B, H, Nq, Nk, dk, dv, _scale(scale, dk), int(bool(causal)),
+                                 dq.ctypes.data, dk_.ctypes.data, dv_.ctypes.data, int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_attn_bwd rejected the problem (code {rc})")
+    return dq, dk_, dv_
 
 
 def max_threads() -> int:

@@ -38,7 +38,8 @@
  *
  * Also returned on request: LSE[i] = m + ln(Z), the log of the softmax
  * denominator in natural-log units, and the full S and P matrices for tiny
- * shapes.
+ * shapes; and the backward pass (dQ, dK, dV for a given dO, see
+ * oracle_attn_bwd below).
  */
 #include <math.h>
 #include <stdint.h>
@@ -210,6 +211,83 @@ int oracle_attn_weights(const void* Q, const void* K, const void* V, int dtype, 
     problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
     if (!S || !P || !O) return 1;
     return run_rows(&p, NULL, B * H * Nq, O, LSE, S, P, 1);
+}
+
+/*
+ * Backward pass: the gradients of a scalar loss through O, given its
+ * gradient dO = dL/dO, by the chain rule through the softmax Jacobian (the
+ * derivative the paper's Stage 5 sets out to take).  Per (b, h) slice, with
+ * w the attention weights of query row i (attend_row's Step IV output):
+ *
+ *   dV[k][c] = sum_i w_i[k] * dO[i][c]
+ *   dP[k]    = sum_c dO[i][c] * V[k][c]                  (per row i)
+ *   D        = sum_k w_i[k] * dP[k]
+ *   dS[k]    = w_i[k] * (dP[k] - D)        (softmax Jacobian: dw/ds = diag(w) - w w^T)
+ *   dQ[i][j] = scale * sum_k dS[k] * K[k][j]
+ *   dK[k][j] = scale * sum_i dS_i[k] * Q[i][j]
+ *
+ * Masked keys have weight 0 and contribute nothing.  One (b, h) slice per
+ * thread, so the sums over i of dK and dV run in increasing i within one
+ * thread.  dO has the storage type of Q, K, V; dQ, dK, dV are fp64 in the
+ * layouts of Q, K, V.
+ */
+int oracle_attn_bwd(const void* Q, const void* K, const void* V, const void* dO, int dtype,
+                    int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                    float scale, int causal, double* dQ, double* dK, double* dV, int nthreads) {
+    problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
+    if (check(&p) || !dO || !dQ || !dK || !dV) return 1;
+    set_threads(nthreads);
+    int nt = 1;
+#ifdef _OPENMP
+    nt = omp_get_max_threads();
+#endif
+    const size_t per = 4 * (size_t)Nk + (size_t)dv;
+    double* scratch = (double*)malloc((size_t)nt * per * sizeof(double));
+    if (!scratch) return 2;
+    for (int64_t x = 0; x < B * H * Nk * dk; ++x) dK[x] = 0.0;
+    for (int64_t x = 0; x < B * H * Nk * dv; ++x) dV[x] = 0.0;
+#pragma omp parallel num_threads(nt)
+    {
+        int tid = 0;
+#ifdef _OPENMP
+        tid = omp_get_thread_num();
+#endif
+        double* s = scratch + (size_t)tid * per;
+        double* e = s + Nk;
+        double* w = e + Nk;
+        double* dp = w + Nk;
+        double* o_row = dp + Nk;
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t bh = 0; bh < B * H; ++bh) {
+            const int64_t k_base = bh * Nk * dk, v_base = bh * Nk * dv;
+            for (int64_t i = 0; i < Nq; ++i) {
+                const int64_t r = bh * Nq + i;
+                attend_row(&p, r, s, e, w, o_row, NULL, NULL, NULL);
+                const int64_t q_row = r * dk, o_off = r * dv;
+                double D = 0.0;
+                for (int64_t k = 0; k < Nk; ++k) {
+                    dp[k] = 0.0;
+                    if (s[k] == -INFINITY) continue;
+                    for (int64_t c = 0; c < dv; ++c)
+                        dp[k] += elem(dO, dtype, o_off + c) * elem(V, dtype, v_base + k * dv + c);
+                    D += w[k] * dp[k];
+                }
+                for (int64_t j = 0; j < dk; ++j) dQ[q_row + j] = 0.0;
+                for (int64_t k = 0; k < Nk; ++k) {
+                    if (s[k] == -INFINITY) continue;
+                    const double ds = w[k] * (dp[k] - D);
+                    for (int64_t j = 0; j < dk; ++j) {
+                        dQ[q_row + j] += (double)scale * ds * elem(K, dtype, k_base + k * dk + j);
+                        dK[k_base + k * dk + j] += (double)scale * ds * elem(Q, dtype, q_row + j);
+                    }
+                    for (int64_t c = 0; c < dv; ++c)
+                        dV[v_base + k * dv + c] += w[k] * elem(dO, dtype, o_off + c);
+                }
+            }
+        }
+    }
+    free(scratch);
+    return 0;
 }
 
 /* Threads OpenMP would use for a call with nthreads <= 0. */

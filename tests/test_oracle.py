@@ -255,3 +255,101 @@ def test_rejects_bad_problems():
         oracle.attention(q, np.zeros((1, 1, 0, 8), np.float32), np.zeros((1, 1, 0, 8), np.float32))
     with pytest.raises(ValueError):
         oracle.attention_rows(q, k, k, [12])               # row out of range
+
+
+# ---- backward pass (gradients through the softmax Jacobian) ----
+
+def _torch_grads(q, k, v, do, scale, causal):
+    """Reference gradients by torch autograd in fp64 on the CPU (explicit softmax)."""
+    def t(a):
+        if a.dtype == np.uint16:
+            return synth.to_torch(a).to(torch.float64)
+        return torch.from_numpy(a).to(torch.float64)
+    tq, tk, tv, tdo = (t(a).requires_grad_(i < 3) for i, a in enumerate((q, k, v, do)))
+    s = scale * (tq @ tk.transpose(-1, -2))
+    if causal:
+        Nq, Nk = q.shape[2], k.shape[2]
+        i = torch.arange(Nq)[:, None]
+        j = torch.arange(Nk)[None, :]
+        s = s.masked_fill(j > i + (Nk - Nq), float("-inf"))
+    o = torch.softmax(s, dim=-1) @ tv
+    o.backward(tdo)
+    return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 5, 5, 8, 8), (2, 3, 7, 11, 16, 16), (1, 2, 9, 13, 64, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_matches_torch_autograd_fp64(shape, causal, dtype):
+    B, H, Nq, Nk, dk, dv = shape
+    q = synth.normal(901, (B, H, Nq, dk), 1.0, dtype)
+    k = synth.normal(902, (B, H, Nk, dk), 1.0, dtype)
+    v = synth.normal(903, (B, H, Nk, dv), 1.0, dtype)
+    do = synth.normal(904, (B, H, Nq, dv), 1.0, dtype)
+    scale = float(np.float32(1 / np.sqrt(dk)))
+    dq, dk_, dv_ = oracle.attention_bwd(q, k, v, do, scale=scale, causal=causal)
+    rq, rk, rv = _torch_grads(q, k, v, do, scale, causal)
+    for a, b in ((dq, rq), (dk_, rk), (dv_, rv)):
+        assert np.max(np.abs(a - b)) < 1e-12
+
+
+def test_backward_central_differences():
+    # L = sum(O * dO).  Inputs are multiples of 2^-8 so that x +- 2^-10 is exact in
+    # fp32; the central difference then has truncation error O(eps^2).
+    rng = np.random.default_rng(5)
+    B, H, Nq, Nk, d = 1, 2, 3, 4, 4
+    q, k, v, do = (np.round(rng.standard_normal(sh) * 256) / 256
+                   for sh in ((B, H, Nq, d), (B, H, Nk, d), (B, H, Nk, d), (B, H, Nq, d)))
+    q, k, v, do = (a.astype(np.float32) for a in (q, k, v, do))
+    scale, eps = 0.5, 2.0 ** -10
+    for causal in (False, True):
+        grads = oracle.attention_bwd(q, k, v, do, scale=scale, causal=causal)
+
+        def loss(qq, kk, vv):
+            return float(np.sum(oracle.attention(qq, kk, vv, scale=scale, causal=causal) * do))
+        for which, g in enumerate(grads):
+            base = (q, k, v)[which]
+            for idx in np.ndindex(base.shape):
+                plus, minus = base.copy(), base.copy()
+                plus[idx] += eps
+                minus[idx] -= eps
+                args_p = [q, k, v]
+                args_m = [q, k, v]
+                args_p[which], args_m[which] = plus, minus
+                fd = (loss(*args_p) - loss(*args_m)) / (2 * eps)
+                assert abs(fd - g[idx]) < 2e-6, (causal, which, idx, fd, g[idx])
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_backward_key_gradients_sum_to_zero(causal):
+    # Each row of dS sums to zero (the softmax Jacobian annihilates constants), so
+    # sum_k dK[k] = scale * sum_i q_i * sum_k dS[i][k] = 0.
+    B, H, Nq, Nk, d = 2, 2, 6, 9, 16
+    q, k, v, do = (synth.normal(910 + i, sh, 1.0, "f32") for i, sh in
+                   enumerate(((B, H, Nq, d), (B, H, Nk, d), (B, H, Nk, d), (B, H, Nq, d))))
+    _, dk_, _ = oracle.attention_bwd(q, k, v, do, causal=causal)
+    assert np.max(np.abs(dk_.sum(axis=2))) < 1e-12
+
+
+def test_backward_constant_values():
+    # Constant V rows: O is that row whatever Q and K are, so dQ = dK = 0, and
+    # dV[k] = sum_i P[i][k] dO[i] with P from the forward oracle.
+    B, H, Nq, Nk, d = 1, 2, 5, 7, 8
+    q = synth.normal(920, (B, H, Nq, d), 1.0, "f32")
+    k = synth.normal(921, (B, H, Nk, d), 1.0, "f32")
+    v = np.broadcast_to(synth.normal(922, (B, H, 1, d), 1.0, "f32"), (B, H, Nk, d)).copy()
+    do = synth.normal(923, (B, H, Nq, d), 1.0, "f32")
+    dq, dk_, dv_ = oracle.attention_bwd(q, k, v, do, causal=True)
+    assert np.max(np.abs(dq)) < 1e-13 and np.max(np.abs(dk_)) < 1e-13
+    _, p, _, _ = oracle.attention_weights(q, k, v, causal=True)
+    ref = np.einsum("bhik,bhic->bhkc", p, do.astype(np.float64))
+    assert np.max(np.abs(dv_ - ref)) < 1e-13
+
+
+def test_backward_rejects_bad_problems():
+    q = synth.normal(930, (1, 1, 4, 8), 1.0, "f32")
+    with pytest.raises(ValueError):
+        oracle.attention_bwd(q, q, q, q[:, :, :3], causal=False)      # dO shape
+    with pytest.raises(ValueError):
+        oracle.attention_bwd(q, q[:, :, :3], q[:, :, :3], q, causal=True)   # causal Nq > Nk
