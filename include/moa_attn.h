@@ -28,7 +28,8 @@
  *    Every tensor pointer must be 16-byte aligned.
  *  - The library allocates no device memory, keeps no state between calls,
  *    never synchronises, and is safe to call from several host threads.  Work
- *    is enqueued on `stream` (at most two kernels); errors raised by kernels
+ *    is enqueued on `stream` (at most two kernels for the forward, three for
+ *    the backward); errors raised by kernels
  *    surface at the caller's next synchronisation.
  *  - Arguments are validated on the host before any HIP call; a rejected call
  *    touches no device memory.
@@ -156,6 +157,68 @@ int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, f
                          const int64_t* v_strides, const int64_t* o_strides, float scale,
                          int causal, int in_dtype, int out_dtype, void* workspace,
                          size_t workspace_bytes, int num_splits, void* stream);
+
+/*
+ * moa_attn_bwd_workspace_bytes -- device workspace a moa_attn_bwd call with
+ * these dimensions needs, in bytes: one fp32 per query row (the row sums D
+ * below), rounded up to 256 bytes.  0 for invalid or unsupported dimensions.
+ */
+size_t moa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
+                                    int64_t dv);
+
+/*
+ * moa_attn_bwd -- gradients of the attention of moa_attn_fwd with respect to
+ * Q, K and V (the backward pass of Sec. "Stage 5: Backward Pass and Full
+ * Training Loop": dL/dQ through dL/dO, V^T, the softmax Jacobian and K, and
+ * likewise for K and V).  With s_ij = scale * <q_i, k_j> over visible j:
+ *
+ *   P_ij  = exp(s_ij - LSE_i)            dP_ij = <dO_i, v_j>
+ *   D_i   = <dO_i, O_i>                  dS_ij = P_ij * (dP_ij - D_i)
+ *   dQ_i  = scale * sum_j dS_ij k_j      dK_j  = scale * sum_i dS_ij q_i
+ *   dV_j  = sum_i P_ij dO_i
+ *
+ * The weights are recomputed from LSE: no n x n score, weight or Jacobian
+ * matrix is ever written to device memory; the only writes are dQ, dK, dV
+ * and the B*H*Nq row sums D in the workspace.
+ *
+ * Q, K, V   the forward's device inputs, bf16 (in_dtype must be MOA_BF16;
+ *           MOA_F32 returns MOA_ERR_UNSUPPORTED), contiguous layouts as for
+ *           moa_attn_fwd.
+ * O         the forward's output, storage type o_dtype (MOA_F32 or
+ *           MOA_BF16), [B][H][Nq][dv].  Only D reads it; an fp32 O gives the
+ *           more accurate D.
+ * dO        device input, bf16 [B][H][Nq][dv]: the gradient of the loss with
+ *           respect to O.
+ * LSE       the forward's LSE output, fp32 [B][H][Nq] (required).
+ * dQ, dK, dV
+ *           device outputs of storage type grad_dtype (MOA_F32 or MOA_BF16),
+ *           shaped like Q, K, V.  Every element is written.
+ * B, H, Nq, Nk, dk, dv, scale, causal
+ *           exactly as passed to the forward call (same rules; dk == dv in
+ *           {64, 128}).
+ * workspace, workspace_bytes
+ *           device scratch of at least moa_attn_bwd_workspace_bytes(...)
+ *           bytes, 16-byte aligned (required when B*H*Nq > 0).
+ * stream    hipStream_t as void*.
+ *
+ * Buffers: dQ, dK, dV and the workspace must not overlap each other or any
+ * input (else MOA_ERR_INVALID_ARG); the inputs may overlap one another.  A
+ * pointer may be NULL only when its tensor has no elements (Q, O, dO, LSE and
+ * dQ when B*H*Nq == 0); every non-NULL pointer must be 16-byte aligned.
+ * Computation: the products S, dP and the three gradient contractions run on
+ * bf16 matrix cores with fp32 accumulation; P and dS are rounded to bf16
+ * before they multiply dO, K and Q; exponentials and D are fp32.  Each
+ * gradient row is owned by one workgroup: no atomics, and the results are
+ * deterministic.  Three kernels are enqueued on `stream`.
+ *
+ * Returns MOA_OK once the work is enqueued (or when B*H == 0: nothing is
+ * launched; when Nq == 0, dK and dV are zero-filled), else a MOA_ERR_* code.
+ */
+int moa_attn_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, void* dQ, void* dK, void* dV, int64_t B, int64_t H, int64_t Nq,
+                 int64_t Nk, int64_t dk, int64_t dv, float scale, int causal, int in_dtype,
+                 int o_dtype, int grad_dtype, void* workspace, size_t workspace_bytes,
+                 void* stream);
 
 /* moa_attn_status_string -- static, human-readable text for a status code. */
 const char* moa_attn_status_string(int status);

@@ -2,7 +2,8 @@
 
 A thin binding over ``libmoa_attn.so``, whose C ABI is ``include/moa_attn.h``.
 The Python names mirror the C entry points (``moa_attn_fwd``,
-``moa_attn_workspace_bytes``, ``moa_attn_num_splits``,
+``moa_attn_fwd_strided``, ``moa_attn_bwd``, ``moa_attn_workspace_bytes``,
+``moa_attn_bwd_workspace_bytes``, ``moa_attn_num_splits``,
 ``moa_attn_status_string``) and only marshal arguments; every step of the
 computation runs in the library's HIP kernels.  ``attn_fwd`` is a convenience
 wrapper for torch tensors (torch supplies device memory and the stream).
@@ -19,7 +20,9 @@ import os
 __all__ = [
     "MOA_OK", "MOA_ERR_INVALID_ARG", "MOA_ERR_UNSUPPORTED", "MOA_ERR_WORKSPACE", "MOA_ERR_HIP",
     "MOA_F32", "MOA_BF16", "MoaAttnError", "moa_attn_fwd", "moa_attn_workspace_bytes",
-    "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd", "LIB_PATH", "lib",
+    "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd",
+    "moa_attn_fwd_strided", "moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "attn_bwd", "LIB_PATH",
+    "lib",
 ]
 
 MOA_OK, MOA_ERR_INVALID_ARG, MOA_ERR_UNSUPPORTED, MOA_ERR_WORKSPACE, MOA_ERR_HIP = 0, 1, 2, 3, 4
@@ -54,6 +57,10 @@ lib.moa_attn_workspace_bytes.argtypes = [_i64] * 6 + [_ci]
 lib.moa_attn_workspace_bytes.restype = _sz
 lib.moa_attn_num_splits.argtypes = [_i64] * 6 + [_ci]
 lib.moa_attn_num_splits.restype = _ci
+lib.moa_attn_bwd_workspace_bytes.argtypes = [_i64] * 6
+lib.moa_attn_bwd_workspace_bytes.restype = _sz
+lib.moa_attn_bwd.argtypes = [_vp] * 9 + [_i64] * 6 + [_f32, _ci, _ci, _ci, _ci, _vp, _sz, _vp]
+lib.moa_attn_bwd.restype = _ci
 lib.moa_attn_status_string.argtypes = [_ci]
 lib.moa_attn_status_string.restype = ctypes.c_char_p
 lib.moa_attn_last_hip_error.argtypes = []
@@ -63,7 +70,7 @@ lib.moa_attn_last_hip_error.restype = ctypes.c_char_p
 class MoaAttnError(RuntimeError):
     def __init__(self, status: int):
         self.status = status
-        msg = f"moa_attn_fwd failed: {moa_attn_status_string(status)} (status {status})"
+        msg = f"moa_attn call failed: {moa_attn_status_string(status)} (status {status})"
         if status == MOA_ERR_HIP:
             msg += f": {moa_attn_last_hip_error()}"
         super().__init__(msg)
@@ -111,6 +118,19 @@ def moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_str
     return int(lib.moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, *ptrs,
                                         float(scale), int(causal), in_dtype, out_dtype, workspace,
                                         workspace_bytes, num_splits, stream))
+
+
+def moa_attn_bwd_workspace_bytes(B, H, Nq, Nk, dk, dv) -> int:
+    return int(lib.moa_attn_bwd_workspace_bytes(B, H, Nq, Nk, dk, dv))
+
+
+def moa_attn_bwd(Q, K, V, O, dO, LSE, dQ, dK, dV, B, H, Nq, Nk, dk, dv, scale, causal, in_dtype,
+                 o_dtype, grad_dtype, workspace, workspace_bytes, stream) -> int:
+    """Raw C call of the backward pass: pointers are ints (device addresses) or None; returns
+    the status."""
+    return int(lib.moa_attn_bwd(Q, K, V, O, dO, LSE, dQ, dK, dV, B, H, Nq, Nk, dk, dv,
+                                float(scale), int(causal), in_dtype, o_dtype, grad_dtype,
+                                workspace, workspace_bytes, stream))
 
 
 def _dtype_code(t):
@@ -175,3 +195,48 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
     if st != MOA_OK:
         raise MoaAttnError(st)
     return (out, lse) if return_lse else out
+
+
+def attn_bwd(q, k, v, o, lse, do, scale=None, causal=False, grad_dtype=None, workspace=None,
+             stream=None):
+    """Gradients (dq, dk, dv) of ``attn_fwd`` on contiguous torch device tensors.
+
+    q, k, v, do: bf16 [B, H, N, d]; o: the forward's output (bf16 or fp32, fp32 gives a
+    more accurate row sum D); lse: the forward's fp32 [B, H, Nq] LSE (``return_lse=True``).
+    ``scale`` and ``causal`` must be the forward's.  ``grad_dtype`` (default fp32) is the
+    storage type of the returned gradients.  Raises ``MoaAttnError`` on a rejected call.
+    """
+    import torch
+    ts = (q, k, v, o, lse, do)
+    for t in ts:
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("attn_bwd takes contiguous device tensors")
+    B, H, Nq, dk = q.shape
+    Nk, dv = k.shape[2], v.shape[3]
+    if (tuple(k.shape) != (B, H, Nk, dk) or tuple(v.shape) != (B, H, Nk, dv)
+            or tuple(o.shape) != (B, H, Nq, dv) or tuple(do.shape) != (B, H, Nq, dv)
+            or tuple(lse.shape) != (B, H, Nq) or lse.dtype != torch.float32):
+        raise ValueError("shape mismatch between q, k, v, o, lse and do")
+    if not (q.dtype == k.dtype == v.dtype == do.dtype):
+        raise TypeError("q, k, v and do must share one dtype")
+    gdt = torch.float32 if grad_dtype is None else grad_dtype
+    if scale is None:
+        scale = 1.0 / math.sqrt(dk)
+    dq = torch.empty_like(q, dtype=gdt)
+    dkk = torch.empty_like(k, dtype=gdt)
+    dvv = torch.empty_like(v, dtype=gdt)
+    ws_bytes = moa_attn_bwd_workspace_bytes(B, H, Nq, Nk, dk, dv)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    st = moa_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(),
+                      lse.data_ptr(), dq.data_ptr(), dkk.data_ptr(), dvv.data_ptr(),
+                      B, H, Nq, Nk, dk, dv, scale, causal, _dtype_code(q.dtype),
+                      _dtype_code(o.dtype), _dtype_code(gdt),
+                      workspace.data_ptr() if workspace is not None else None,
+                      workspace.numel() * workspace.element_size() if workspace is not None else 0,
+                      stream.cuda_stream)
+    if st != MOA_OK:
+        raise MoaAttnError(st)
+    return dq, dkk, dvv

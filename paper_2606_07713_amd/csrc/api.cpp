@@ -243,6 +243,74 @@ int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, f
                     num_splits, stream);
 }
 
+size_t moa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
+                                    int64_t dv) {
+    if (!dims_ok(B, H, Nq, Nk, dk, dv)) return 0;
+    if (!head_supported(dk, dv) || !sizes_fit(B, H, Nq, Nk, dk)) return 0;
+    return align256((size_t)(B * H) * (size_t)Nq * sizeof(float));
+}
+
+int moa_attn_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, void* dQ, void* dK, void* dV, int64_t B, int64_t H, int64_t Nq,
+                 int64_t Nk, int64_t dk, int64_t dv, float scale, int causal, int in_dtype,
+                 int o_dtype, int grad_dtype, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+    // ---- validation: no HIP call happens before all of it has passed
+    if (!dims_ok(B, H, Nq, Nk, dk, dv)) return MOA_ERR_INVALID_ARG;
+    // A pointer may be NULL only when its tensor has no elements.
+    const bool has_q = B * H * Nq > 0, has_k = B * H > 0;
+    if ((has_k && (!K || !V || !dK || !dV)) || (has_q && (!Q || !O || !dO || !LSE || !dQ)))
+        return MOA_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return MOA_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1) return MOA_ERR_INVALID_ARG;
+    if (causal && Nq > Nk) return MOA_ERR_INVALID_ARG;
+    for (int t : {in_dtype, o_dtype, grad_dtype})
+        if (t != MOA_F32 && t != MOA_BF16) return MOA_ERR_INVALID_ARG;
+    const void* ptrs[] = {Q, K, V, O, dO, LSE, dQ, dK, dV};
+    for (const void* q : ptrs)
+        if (!aligned16(q)) return MOA_ERR_INVALID_ARG;
+    if (workspace && !aligned16(workspace)) return MOA_ERR_INVALID_ARG;
+    if (in_dtype != MOA_BF16) return MOA_ERR_UNSUPPORTED;
+    if (!head_supported(dk, dv)) return MOA_ERR_UNSUPPORTED;
+    if (!sizes_fit(B, H, Nq, Nk, dk)) return MOA_ERR_UNSUPPORTED;
+
+    const int64_t bh = B * H;
+    const size_t qn = (size_t)(bh * Nq * dk) * 2, kn = (size_t)(bh * Nk * dk) * 2;
+    const size_t vn = (size_t)(bh * Nk * dv) * 2, on = (size_t)(bh * Nq * dv) * (o_dtype == MOA_F32 ? 4 : 2);
+    const size_t gn = (size_t)(bh * Nq * dv) * 2, ln = (size_t)(bh * Nq) * sizeof(float);
+    const size_t ges = grad_dtype == MOA_F32 ? 4 : 2;
+    const size_t dqn = (size_t)(bh * Nq * dk) * ges, dkn = (size_t)(bh * Nk * dk) * ges;
+    const size_t dvn = (size_t)(bh * Nk * dv) * ges;
+    const size_t need = moa_attn_bwd_workspace_bytes(B, H, Nq, Nk, dk, dv);
+    if (need && (!workspace || workspace_bytes < need)) return MOA_ERR_WORKSPACE;
+    struct Buf { const void* p; size_t n; };
+    const Buf ins[] = {{Q, qn}, {K, kn}, {V, vn}, {O, on}, {dO, gn}, {LSE, ln}};
+    const Buf outs[] = {{dQ, dqn}, {dK, dkn}, {dV, dvn}, {workspace, need}};
+    for (int i = 0; i < 4; ++i) {
+        for (const Buf& b : ins)
+            if (overlaps(outs[i].p, outs[i].n, b.p, b.n)) return MOA_ERR_INVALID_ARG;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return MOA_ERR_INVALID_ARG;
+    }
+    if (bh == 0) return MOA_OK;
+
+    moa::BwdProblem p;
+    p.q = Q; p.k = K; p.v = V; p.o = O; p.dout = dO; p.lse = LSE;
+    p.dsum = static_cast<float*>(workspace);
+    p.dq = dQ; p.dk = dK; p.dv = dV;
+    p.bh = (int)bh; p.nq = (int)Nq; p.nk = (int)Nk; p.d = (int)dk;
+    p.scale = scale;
+    p.causal = causal != 0;
+    p.o_bf16 = o_dtype == MOA_BF16;
+    p.grad_bf16 = grad_dtype == MOA_BF16;
+    const hipError_t e = moa::launch_bwd(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = hipGetErrorName(e);
+        return MOA_ERR_HIP;
+    }
+    return MOA_OK;
+}
+
 const char* moa_attn_last_hip_error(void) { return g_last_hip_error; }
 
 const char* moa_attn_status_string(int status) {

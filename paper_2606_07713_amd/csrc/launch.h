@@ -56,6 +56,31 @@ hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream);
 // `ws` holds bh*splits*(d + 2) floats.
 hipError_t launch_decode(const Problem& p, int splits, float* ws, hipStream_t stream);
 
+// One backward problem after validation (contiguous [B][H][N][d] tensors).
+// q, k, v, dout: bf16; o: bf16 or fp32; lse: fp32 natural-log LSE of the
+// forward; dsum: workspace of bh*nq floats; dq, dk, dv: fp32 or bf16.
+struct BwdProblem {
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* o;
+    const void* dout;
+    const float* lse;
+    float* dsum;
+    void* dq;
+    void* dk;
+    void* dv;
+    int bh;
+    int nq, nk, d;
+    float scale;
+    bool causal;
+    bool o_bf16;
+    bool grad_bf16;
+};
+
+// Backward: row-dot kernel (D), dQ kernel, dK/dV kernel, in stream order.
+hipError_t launch_bwd(const BwdProblem& p, hipStream_t stream);
+
 // Row-tile size of the bf16 prefill kernel (queries per workgroup).
 constexpr int kPrefillBf16RowsPerBlock = 256;
 // Row-tile size of the fp32 prefill kernel.

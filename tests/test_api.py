@@ -20,8 +20,9 @@ def _declared_functions():
 
 def test_header_declares_the_entry_points():
     names = _declared_functions()
-    assert names == ["moa_attn_fwd", "moa_attn_fwd_strided", "moa_attn_last_hip_error",
-                     "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_workspace_bytes"]
+    assert names == ["moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "moa_attn_fwd",
+                     "moa_attn_fwd_strided", "moa_attn_last_hip_error", "moa_attn_num_splits",
+                     "moa_attn_status_string", "moa_attn_workspace_bytes"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -139,6 +140,55 @@ def test_strided_accepts_common_layouts_without_gpu_work():
                          q_strides=(4 * 8 * 72, 8 * 72, 72)) == moa.MOA_OK
     # A NULL stride array means the contiguous layout of moa_attn_fwd.
     assert _call_strided(B=0) == _call(B=0) == moa.MOA_OK
+
+
+G, DQ, DK, DV, L = 6 << 40, 7 << 40, 8 << 40, 9 << 40, 10 << 40
+
+
+def _call_bwd(**kw):
+    args = dict(Q=A, K=BUF, V=C, O=D, dO=G, LSE=L, dQ=DQ, dK=DK, dV=DV, B=2, H=4, Nq=8, Nk=8,
+                dk=64, dv=64, scale=0.125, causal=0, in_dtype=moa.MOA_BF16, o_dtype=moa.MOA_F32,
+                grad_dtype=moa.MOA_F32, workspace=W, workspace_bytes=1 << 20, stream=None)
+    args.update(kw)
+    return moa.moa_attn_bwd(**args)
+
+
+def test_bwd_workspace_bytes():
+    # one fp32 row sum per query row, rounded up to 256 bytes
+    assert moa.moa_attn_bwd_workspace_bytes(2, 16, 4096, 4096, 128, 128) == 2 * 16 * 4096 * 4
+    assert moa.moa_attn_bwd_workspace_bytes(1, 1, 3, 8, 64, 64) == 256
+    assert moa.moa_attn_bwd_workspace_bytes(1, 1, 0, 8, 64, 64) == 0
+    assert moa.moa_attn_bwd_workspace_bytes(1, 1, 8, 8, 96, 96) == 0      # unsupported head
+    assert moa.moa_attn_bwd_workspace_bytes(1, 1, 8, 0, 64, 64) == 0      # invalid Nk
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Q=None), 1), (dict(dO=None), 1), (dict(LSE=None), 1), (dict(O=None), 1),
+    (dict(dQ=None), 1), (dict(dK=None), 1), (dict(dV=None), 1),
+    (dict(B=-1), 1), (dict(Nk=0), 1), (dict(scale=float("nan")), 1),
+    (dict(causal=1, Nq=9, Nk=8), 1), (dict(causal=3), 1),
+    (dict(o_dtype=5), 1), (dict(grad_dtype=5), 1), (dict(in_dtype=5), 1),
+    (dict(dO=G + 8), 1), (dict(dK=DK + 4), 1), (dict(workspace=W + 8), 1),
+    (dict(dQ=A + 64), 1),                              # dQ overlaps Q
+    (dict(dV=DK + 64), 1),                             # dV overlaps dK
+    (dict(workspace=L), 1),                            # workspace overlaps LSE
+    (dict(dK=D), 1),                                   # dK overlaps O
+    (dict(in_dtype=0), 2),                             # fp32 inputs: not offered
+    (dict(dk=96, dv=96), 2), (dict(dk=64, dv=128), 2),
+    (dict(workspace=None), 3), (dict(workspace_bytes=16), 3),
+])
+def test_bwd_validation_rejects_before_any_gpu_work(kw, status):
+    assert _call_bwd(**kw) == status
+
+
+def test_bwd_empty_batch_is_a_no_op():
+    assert _call_bwd(B=0) == moa.MOA_OK
+    assert _call_bwd(H=0, workspace=None, workspace_bytes=0) == moa.MOA_OK
+    # tensors without elements may be NULL
+    assert _call_bwd(B=0, **{n: None for n in ("Q", "K", "V", "O", "dO", "LSE", "dQ", "dK",
+                                                 "dV", "workspace")}) == moa.MOA_OK
+    # with Nq == 0 the query-side tensors may be NULL, but dK and dV are still written
+    assert _call_bwd(Nq=0, Q=None, O=None, dO=None, LSE=None, dQ=None, dK=None) == 1
 
 
 def test_empty_problems_are_no_ops():
