@@ -14,8 +14,11 @@ TFLOP/s (prefill, matrix-core bound) and GB/s (decode, HBM bound) against the
 MI355X peaks.  The fp64 CPU oracle is timed on a bounded sample of the
 prefill workload on the host's cores as a reported baseline.
 
+The backward pass of the prefill workload (dQ, dK, dV from the forward's O and
+LSE for a seeded dO) is timed in the same run and reported under "backward".
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline] [--no-decode] [--calibrate-copy MIB]
+                       [--no-cpu-baseline] [--no-decode] [--no-backward] [--calibrate-copy MIB]
 """
 from __future__ import annotations
 
@@ -48,6 +51,12 @@ def visible_pairs(w) -> int:
 def algorithmic_flops(w) -> float:
     """Matrix-product flops over visible pairs: 2*dk for Q.K^T plus 2*dv for P.V."""
     return 2.0 * (w.dk + w.dv) * visible_pairs(w)
+
+
+def backward_flops(w) -> float:
+    """Matrix-product flops of the gradients over visible pairs: the recomputed scores
+    (2*dk), dP = dO V^T (2*dv), dV (2*dv), dQ and dK (2*dk each) -- 2.5x the forward's."""
+    return 2.0 * (3 * w.dk + 2 * w.dv) * visible_pairs(w)
 
 
 def compulsory_bytes(w, out_bytes: int) -> int:
@@ -154,6 +163,8 @@ def main(argv=None):
     ap.add_argument("--decode-workload", default=DEFAULT_DECODE)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the timing of the backward pass (reported under \"backward\")")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain copy kernel of MIB MiB (read MIB, "
                          "write MIB) so profiler byte counters can be scaled against it")
@@ -257,6 +268,29 @@ def main(argv=None):
                          if args.layout == "bhnd" else None},
         }
         print(f"# decode {wd.name}: {msd:.4f} ms/call, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
+
+    if not args.no_backward and w.dtype == "bf16" and args.layout == "bhnd":
+        # Gradients of the same workload for a seeded dO, from the forward's O and LSE.
+        tq, tk, tv = (synth.to_torch(a, dev) for a in host)
+        o, lse = moa.attn_fwd(tq, tk, tv, scale=w.scale, causal=w.causal, return_lse=True)
+        do = synth.to_torch(synth.normal(7919, (w.B, w.H, w.Nq, w.dv), 1.0, "bf16"), dev)
+        ws_b = moa.moa_attn_bwd_workspace_bytes(w.B, w.H, w.Nq, w.Nk, w.dk, w.dv)
+        ws_bwd = torch.empty(max(ws_b, 1), dtype=torch.uint8, device=dev)
+
+        def call_bwd():
+            moa.attn_bwd(tq, tk, tv, o, lse, do, scale=w.scale, causal=w.causal,
+                         grad_dtype=torch.bfloat16, workspace=ws_bwd if ws_b else None,
+                         stream=stream)
+        steps_b = max(1, args.steps // 5)
+        msb = time_calls(call_bwd, steps_b, min(args.warmup, 2), stream)
+        fb = backward_flops(w)
+        line["backward"] = {"workload": w.name, "ms_per_call": round(msb, 4), "steps": steps_b,
+                            "value": round(fb / (msb * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+                            "flop_per_call": fb, "grad_dtype": "bf16",
+                            "frac": round(fb / (msb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        print(f"# backward {w.name}: {msb:.4f} ms/call, {fb / (msb * 1e-3) / 1e12:.1f} TFLOP/s",
+              file=sys.stderr, flush=True)
+        del o, lse, do, ws_bwd
 
     line["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(w, host)
     print(json.dumps(line), flush=True)

@@ -43,3 +43,9 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_backward_flops_are_two_and_a_half_forwards():
+    for name in ("causal_long_b1h32_n16384_d128_bf16_qk_sigma3", "mha_b4h8_n1024_d64_bf16"):
+        w = synth.WORKLOADS[name]
+        assert bench.backward_flops(w) == 2.5 * bench.algorithmic_flops(w)
