@@ -13,9 +13,10 @@
  * computed as in the Denotational Normal Form (eqs. dnf_attn, output_dnf):
  * no transposed-K buffer, no score matrix and no softmax temporary is ever
  * written to device memory.  The only device-memory writes of a prefill call
- * are O (and LSE when requested); a decode call (Nq == 1) additionally writes
- * per-split partial results of size O(B*H*splits*dv) into the caller's
- * workspace.
+ * are O (and LSE when requested); a call that splits its keys across
+ * workgroups (decode, Nq == 1; prefill on grids too small to fill the GPU)
+ * additionally writes per-split partial results of size
+ * O(B*H*Nq*splits*dv) into the caller's workspace.
  *
  * Conventions shared by all entry points
  *  - Plain C types only; no HIP or framework types appear here.  `stream` is a
@@ -64,18 +65,26 @@ enum {
  * moa_attn_workspace_bytes -- device workspace a moa_attn_fwd call with the
  * same arguments needs, in bytes (0 when none).
  *
- * Only decode-shaped calls (Nq == 1) need a workspace: they split the key
- * range into `num_splits` chunks (0 = the library's choice, which this
- * function then reports for) and combine the partial softmax results in a
- * second pass; the workspace holds those partials, fp32, for B*H*splits rows.
- * Returns 0 for prefill-shaped calls and for invalid dimensions.
+ * Calls that split the key range into chunks (`num_splits`; 0 = the
+ * library's choice, which this function then reports for) and combine the
+ * partial softmax results in a second pass need a workspace for those
+ * partials: B*H*Nq*splits rows of dv + 2 fp32 values, rounded up to 256
+ * bytes.  Decode-shaped calls (Nq == 1) always split.  bf16 prefill calls
+ * (Nq > 1) split when the library's choice (or `num_splits` > 1) says so:
+ * automatically only for grids too small to fill the GPU (fewer than 128
+ * tiles of 256 queries over all B*H slices, and at least 2048 keys), where
+ * splits * (128-query tiles) approaches 256 workgroups with at least 1024
+ * keys per split.  fp32 prefill never splits (its call ignores the
+ * workspace).  Returns 0 when the call does not split and for invalid
+ * dimensions.
  */
 size_t moa_attn_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
                                 int64_t dv, int num_splits);
 
 /*
- * moa_attn_num_splits -- the number of key splits a decode-shaped call
- * (Nq == 1) with these arguments will use (1 for prefill-shaped calls).
+ * moa_attn_num_splits -- the number of key splits a call with these
+ * arguments will use when given moa_attn_workspace_bytes(...) of workspace
+ * (decode-shaped calls, and bf16 prefill; 1 = no split).
  */
 int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
                         int num_splits);
@@ -100,11 +109,16 @@ int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk
  *           j <= i + (Nk - Nq) (bottom-right aligned; j <= i when Nq == Nk).
  *           Requires Nq <= Nk, so no query row is fully masked.
  * workspace, workspace_bytes
- *           device scratch for decode-shaped calls; at least
+ *           device scratch for calls that split their keys; at least
  *           moa_attn_workspace_bytes(...) bytes, 16-byte aligned, not
- *           overlapping any tensor.  May be NULL/0 when that is 0.
+ *           overlapping any tensor.  Required for decode-shaped calls and
+ *           for bf16 prefill with num_splits > 1 (else MOA_ERR_WORKSPACE);
+ *           a bf16 prefill call with num_splits == 0 whose workspace is
+ *           missing or too small runs in one pass instead.  May be NULL/0
+ *           when moa_attn_workspace_bytes(...) is 0.
  * num_splits
- *           decode key splits (0 = library's choice, else 1..256).
+ *           key splits across workgroups (0 = library's choice, else
+ *           1..256; 1 = no split for prefill).  Ignored by fp32 prefill.
  * stream    hipStream_t as void*.
  *
  * Computation: inner products and softmax statistics in fp32 from exact

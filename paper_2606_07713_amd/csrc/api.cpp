@@ -15,6 +15,13 @@ constexpr int kMaxSplits = 256;
 // automatic split choice aims for (several waves of workgroups per CU).
 constexpr int64_t kMinKeysPerSplit = 256;
 constexpr int64_t kTargetDecodeBlocks = 8192;
+// Prefill (Nq > 1, bf16): keys are split across workgroups when fewer than
+// kPrefillSplitBelowItems 256-query items exist (half the 256 compute units
+// of an MI355X), aiming at kPrefillTargetBlocks 128-query split items, each
+// split covering at least kMinKeysPerPrefillSplit keys.
+constexpr int64_t kPrefillSplitBelowItems = 128;
+constexpr int64_t kPrefillTargetBlocks = 256;
+constexpr int64_t kMinKeysPerPrefillSplit = 1024;
 
 bool dims_ok(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv) {
     return B >= 0 && H >= 0 && Nq >= 0 && Nk >= 1 && dk >= 1 && dv >= 1;
@@ -44,10 +51,32 @@ int pick_splits(int64_t bh, int64_t Nk, int requested) {
     return (int)s;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int pick_prefill_splits(int64_t bh, int64_t Nq, int64_t Nk, int requested) {
+    if (requested > 0) return requested;
+    if (bh * ((Nq + 255) / 256) >= kPrefillSplitBelowItems) return 1;
+    const int64_t items = bh * ((Nq + 127) / 128);
+    int64_t s = (kPrefillTargetBlocks + items - 1) / items;
+    const int64_t cap = Nk / kMinKeysPerPrefillSplit;
+    if (s > cap) s = cap;
+    if (s > kMaxSplits) s = kMaxSplits;
+    if (s < 1) s = 1;
+    return (int)s;
+}
+
+// Split-K work items (128-query tiles x splits per head slice) must fit the
+// kernels' 32-bit counters.
+bool prefill_splits_fit(int64_t bh, int64_t Nq, int splits) {
+    return bh * ((Nq + 127) / 128) * splits <= std::numeric_limits<int32_t>::max();
+}
+
+size_t prefill_ws_bytes(int64_t bh, int64_t Nq, int64_t d, int splits) {
+    return align256((size_t)bh * (size_t)Nq * (size_t)splits * (size_t)(d + 2) * sizeof(float));
+}
+
 // Name of the HIP error behind the last MOA_ERR_HIP returned on this thread.
 thread_local const char* g_last_hip_error = "hipSuccess";
-
-size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 size_t decode_ws_bytes(int64_t bh, int64_t d, int splits) {
     return align256((size_t)bh * (size_t)splits * (size_t)(d + 2) * sizeof(float));
@@ -111,19 +140,24 @@ extern "C" {
 
 int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
                         int num_splits) {
-    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq != 1) return 1;
+    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq == 0) return 1;
     if (num_splits < 0 || num_splits > kMaxSplits) return 1;
-    return pick_splits(B * H, Nk, num_splits);
+    if (Nq == 1) return pick_splits(B * H, Nk, num_splits);
+    if (B * H == 0) return 1;
+    return pick_prefill_splits(B * H, Nq, Nk, num_splits);
 }
 
 size_t moa_attn_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
                                 int64_t dv, int num_splits) {
-    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq != 1) return 0;
+    if (!dims_ok(B, H, Nq, Nk, dk, dv) || Nq == 0) return 0;
     if (num_splits < 0 || num_splits > kMaxSplits) return 0;
     if (!head_supported(dk, dv) || !sizes_fit(B, H, Nq, Nk, dk)) return 0;
     const int64_t bh = B * H;
     if (bh == 0) return 0;
-    return decode_ws_bytes(bh, dk, pick_splits(bh, Nk, num_splits));
+    if (Nq == 1) return decode_ws_bytes(bh, dk, pick_splits(bh, Nk, num_splits));
+    const int s = pick_prefill_splits(bh, Nq, Nk, num_splits);
+    if (s <= 1 || !prefill_splits_fit(bh, Nq, s)) return 0;
+    return prefill_ws_bytes(bh, Nq, dk, s);
 }
 
 }  // extern "C"
@@ -183,6 +217,19 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
         splits = pick_splits(bh, Nk, num_splits);
         need = decode_ws_bytes(bh, dk, splits);
         if (!workspace || workspace_bytes < need) return MOA_ERR_WORKSPACE;
+    } else if (!decode && bh > 0 && Nq > 0 && in_dtype == MOA_BF16) {
+        // Split-K prefill: explicitly requested splits need the workspace;
+        // the automatic choice falls back to one pass without it.
+        splits = pick_prefill_splits(bh, Nq, Nk, num_splits);
+        if (splits > 1 && !prefill_splits_fit(bh, Nq, splits)) return MOA_ERR_UNSUPPORTED;
+        need = splits > 1 ? prefill_ws_bytes(bh, Nq, dk, splits) : 0;
+        if (need && (!workspace || workspace_bytes < need)) {
+            if (num_splits > 1) return MOA_ERR_WORKSPACE;
+            splits = 1;
+            need = 0;
+        }
+    }
+    if (need) {
         const size_t wn = need;
         if (overlaps(workspace, wn, O, on) || overlaps(workspace, wn, Q, qn) ||
             overlaps(workspace, wn, K, kn) || overlaps(workspace, wn, V, vn) ||
@@ -203,6 +250,8 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
     p.lay.vb = sv.b; p.lay.vh = sv.h; p.lay.vr = (int)sv.r;
     p.lay.ob = so.b; p.lay.oh = so.h; p.lay.orow = (int)so.r;
     p.lay.H = (int)H;
+    p.splits = splits;
+    p.ws = static_cast<float*>(workspace);
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     hipError_t e;

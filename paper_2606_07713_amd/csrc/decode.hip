@@ -172,40 +172,6 @@ __global__ __launch_bounds__(THREADS) void decode_split_kernel(
     }
 }
 
-// a9: exact merge of the per-chunk states of one (batch*head).
-template <int D, bool OUT_BF16>
-__global__ __launch_bounds__(64) void decode_combine_kernel(
-    const float* __restrict__ ws_acc, const float* __restrict__ ws_ml, void* __restrict__ Out,
-    float* __restrict__ LSE, int splits, Layout lay) {
-    constexpr int PER = D / 64;
-    const int bh = blockIdx.x;
-    const int lane = threadIdx.x;
-    const float* ml = ws_ml + (size_t)bh * splits * 2;
-    const float* ac = ws_acc + (size_t)bh * splits * D;
-    float M = kNegInf;
-    for (int s = 0; s < splits; ++s) M = fmaxf(M, ml[2 * s]);
-    float L = 0.0f, o[PER];
-#pragma unroll
-    for (int e = 0; e < PER; ++e) o[e] = 0.0f;
-    for (int s = 0; s < splits; ++s) {
-        const float ms = ml[2 * s];
-        const float w = (ms == kNegInf) ? 0.0f : exp2_hw(ms - M);
-        L += w * ml[2 * s + 1];
-#pragma unroll
-        for (int e = 0; e < PER; ++e) o[e] += w * ac[(size_t)s * D + e * 64 + lane];
-    }
-    const float inv = 1.0f / L;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) {
-        const size_t idx = (size_t)head_offset(bh, lay.H, lay.ob, lay.oh) + e * 64 + lane;
-        if (OUT_BF16)
-            static_cast<u16*>(Out)[idx] = (u16)f32_to_bf16_bits(o[e] * inv);
-        else
-            static_cast<float*>(Out)[idx] = o[e] * inv;
-    }
-    if (LSE != nullptr && lane == 0) LSE[bh] = (M + __log2f(L)) * kLn2;
-}
-
 template <typename T, int D>
 hipError_t launch_t(const Problem& p, int splits, float* ws, hipStream_t stream) {
     const int kps = (p.nk + splits - 1) / splits;
@@ -217,13 +183,8 @@ hipError_t launch_t(const Problem& p, int splits, float* ws, hipStream_t stream)
                                  static_cast<const T*>(p.v), ws_acc, ws_ml, p.nk, splits, kps,
                                  p.scale * kLog2e, p.lay);
     if (e != hipSuccess) return e;
-    if (p.out_bf16)
-        return launch_kernel(decode_combine_kernel<D, true>, dim3(p.bh), dim3(64), stream,
-                             static_cast<const float*>(ws_acc), static_cast<const float*>(ws_ml),
-                             p.o, p.lse, splits, p.lay);
-    return launch_kernel(decode_combine_kernel<D, false>, dim3(p.bh), dim3(64), stream,
-                         static_cast<const float*>(ws_acc), static_cast<const float*>(ws_ml), p.o,
-                         p.lse, splits, p.lay);
+    // a9: exact merge of the per-chunk states (one query row per batch*head).
+    return launch_split_combine(p, splits, ws_acc, ws_ml, stream);
 }
 
 }  // namespace

@@ -32,6 +32,10 @@ struct Problem {
     bool in_bf16;
     bool out_bf16;
     Layout lay;
+    // Key splits of a split-K launch (1 = none) and its fp32 workspace:
+    // partial states [bh * nq][splits][d] followed by [bh * nq][splits][2].
+    int splits;
+    float* ws;
 };
 
 // True if every tensor of `p` has the contiguous [B][H][N][d] strides.
@@ -55,6 +59,12 @@ hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream);
 // Decode (Nq == 1): split-K partial kernel + combine kernel.
 // `ws` holds bh*splits*(d + 2) floats.
 hipError_t launch_decode(const Problem& p, int splits, float* ws, hipStream_t stream);
+
+// Second pass of a split-K launch: merges the `splits` partial states of each
+// of the bh * nq query rows (ws_acc [rows][splits][d], ws_ml [rows][splits][2])
+// into O (and LSE when p.lse is set).
+hipError_t launch_split_combine(const Problem& p, int splits, const float* ws_acc,
+                                const float* ws_ml, hipStream_t stream);
 
 // One backward problem after validation (contiguous [B][H][N][d] tensors).
 // q, k, v, dout: bf16; o: bf16 or fp32; lse: fp32 natural-log LSE of the

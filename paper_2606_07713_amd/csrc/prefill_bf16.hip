@@ -63,11 +63,20 @@ __device__ __forceinline__ void wait_loads_to_lds() {
 //   groups in the same phase), and group 1 hands its softmax state (m, l, O)
 //   to group 0 through LDS at the end for an exact merge.  Used when the
 //   ping-pong grid is too small to fill the GPU.
-template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED>
+// PARTIAL = true (with KSPLIT): split-K across workgroups for grids smaller
+//   still.  Work item = (batch*head, query tile, key split s of n_splits):
+//   the item covers the s-th of n_splits equal shares of the query tile's
+//   visible key tiles and, instead of O, writes its partial state -- the
+//   reference m (log2 units), the denominator l and the un-normalised output
+//   acc -- to Out = ws_acc [bh*Nq][n_splits][D] and LSE = ws_ml
+//   [bh*Nq][n_splits][2]; launch_split_combine merges the splits.  A share
+//   with no key visible to a row leaves (m, l, acc) = (-inf, 0, 0).
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED, bool PARTIAL = false>
 __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
     void* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_bh, int n_qtiles, float c,
-    Layout L) {
+    Layout L, int n_splits) {
+    static_assert(!PARTIAL || KSPLIT, "split-K items use the key-split layout");
     const Addr<D, STRIDED> A{L, Nq, Nk};
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
@@ -114,6 +123,11 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     for (int item = 0;; ++item) {
     int bh, qt;
     if (!item_of(blockIdx.x, item, gridDim.x, n_bh, n_qtiles, CAUSAL, bh, qt)) break;
+    int split = 0;                 // key share of a split-K item
+    if constexpr (PARTIAL) {
+        split = qt % n_splits;
+        qt /= n_splits;
+    }
     const int q0 = qt * BMQ;
 
     const u16* Qh = Q + A.q_head(bh);
@@ -139,9 +153,15 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     int kv_end = Nk;
     if (CAUSAL) kv_end = min(Nk, q0 + BMQ + off);
     const int n_kt = (kv_end + BN - 1) / BN;
-    const int n_first = KSPLIT ? (n_kt + 1) / 2 : n_kt;      // tiles of stream 0
-    const int g_start = (KSPLIT && grp == 1) ? n_first : 0;   // first global tile of the stream
-    const int g_count = (KSPLIT && grp == 1) ? n_kt - n_first : n_first;
+    int t_lo = 0, n_range = n_kt;                             // this item's key tiles
+    if constexpr (PARTIAL) {
+        const int share = (n_kt + n_splits - 1) / n_splits;
+        t_lo = min(n_kt, split * share);
+        n_range = min(n_kt, t_lo + share) - t_lo;
+    }
+    const int n_first = KSPLIT ? (n_range + 1) / 2 : n_range;   // tiles of stream 0
+    const int g_start = t_lo + ((KSPLIT && grp == 1) ? n_first : 0);   // first global tile of the stream
+    const int g_count = (KSPLIT && grp == 1) ? n_range - n_first : n_first;
     const int n_iter = n_first;                               // slots every wave walks through
     const int wave_q_first = q0 + qw * 32;
     int w_end = n_kt;                                         // global tiles this wave needs
@@ -414,6 +434,28 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         }
     }
 
+    // ---- a8 (split-K): the partial state of this key share, un-normalised,
+    // for the combine pass.
+    if constexpr (PARTIAL) {
+    if (grp == 0) {
+    const float l_tot = half_sum(l_run);
+    if (qrow < Nq) {
+        const size_t prow = ((size_t)bh * Nq + qrow) * n_splits + split;
+        float* acc_out = static_cast<float*>(Out) + prow * D;
+#pragma unroll
+        for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(acc_out + dv_of<D>(b, g * 8 + half * 4)) =
+                    make_float4(oacc[b][g * 4 + 0], oacc[b][g * 4 + 1], oacc[b][g * 4 + 2],
+                                oacc[b][g * 4 + 3]);
+        if (half == 0) {
+            LSE[prow * 2 + 0] = m_run;
+            LSE[prow * 2 + 1] = l_tot;
+        }
+    }
+    }
+    } else {
     // ---- a7: epilogue, O = acc / l: the only device-memory write (key
     // split: by group 0, which holds the merged state).
     if (!KSPLIT || grp == 0) {
@@ -441,6 +483,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
     }
     }
+    }
     // Every wave is done with this item's LDS before the next item's first
     // tile load lands there.
     __syncthreads();
@@ -454,10 +497,12 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
 constexpr long long kPingPongFromItems = 1024;
 
 // One persistent launch: as many workgroups as the device holds at once, at
-// most one per work item.
-template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED>
-hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, hipStream_t stream) {
-    auto kernel = prefill_bf16_kernel<D, CAUSAL, OUT_BF16, KSPLIT, STRIDED>;
+// most one per work item.  `n_qtiles` counts query tiles times key splits;
+// `out` and `lse` are O and LSE, or the two partial-state arrays (PARTIAL).
+template <int D, bool CAUSAL, bool OUT_BF16, bool KSPLIT, bool STRIDED, bool PARTIAL = false>
+hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, void* out, float* lse,
+                             int n_splits, hipStream_t stream) {
+    auto kernel = prefill_bf16_kernel<D, CAUSAL, OUT_BF16, KSPLIT, STRIDED, PARTIAL>;
     static const int per_cu = [&] {
         int n = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, THREADS, 0) != hipSuccess) n = 1;
@@ -470,23 +515,33 @@ hipError_t launch_persistent(const Problem& p, int n_qtiles, float c, hipStream_
     const unsigned grid = (unsigned)std::min<long long>(items, (long long)cus * per_cu);
     return launch_kernel(kernel, dim3(grid), dim3(THREADS), stream,
                          static_cast<const u16*>(p.q), static_cast<const u16*>(p.k),
-                         static_cast<const u16*>(p.v), p.o, p.lse, p.nq, p.nk, p.bh, n_qtiles, c,
-                         p.lay);
+                         static_cast<const u16*>(p.v), out, lse, p.nq, p.nk, p.bh, n_qtiles, c,
+                         p.lay, n_splits);
 }
 
 template <int D, bool CAUSAL, bool OUT_BF16, bool STRIDED>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const float c = p.scale * kLog2e;
     const int qt_pp = (p.nq + BM - 1) / BM;
+    const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
+    if (p.splits > 1) {
+        // Split-K: partial states of every key share, then the exact merge.
+        float* ws_acc = p.ws;
+        float* ws_ml = p.ws + (size_t)p.bh * p.nq * p.splits * D;
+        const hipError_t e = launch_persistent<D, CAUSAL, false, true, STRIDED, true>(
+            p, qt_ks * p.splits, c, ws_acc, ws_ml, p.splits, stream);
+        if (e != hipSuccess) return e;
+        return launch_split_combine(p, p.splits, ws_acc, ws_ml, stream);
+    }
     const long long items = (long long)p.bh * qt_pp;
     if (items >= kPingPongFromItems || p.nk <= BN)
-        return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, stream);
+        return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, p.o, p.lse, 1,
+                                                                      stream);
     int cus = 0;
     const hipError_t e = device_cus(stream, cus);
     if (e != hipSuccess) return e;
     if (items >= cus) return launch_prefill_bf16_pipe(p, stream);
-    const int qt_ks = (p.nq + BM / 2 - 1) / (BM / 2);
-    return launch_persistent<D, CAUSAL, OUT_BF16, true, STRIDED>(p, qt_ks, c, stream);
+    return launch_persistent<D, CAUSAL, OUT_BF16, true, STRIDED>(p, qt_ks, c, p.o, p.lse, 1, stream);
 }
 
 template <int D, bool STRIDED>

@@ -54,9 +54,22 @@ def test_status_strings():
 
 
 def test_workspace_and_splits():
-    # prefill-shaped calls need no workspace
+    # prefill grids that fill the GPU run in one pass, without workspace
     assert moa.moa_attn_workspace_bytes(2, 16, 4096, 4096, 128, 128, 0) == 0
     assert moa.moa_attn_num_splits(2, 16, 4096, 4096, 128, 128, 0) == 1
+    assert moa.moa_attn_num_splits(1, 32, 16384, 16384, 128, 128, 0) == 1
+    assert moa.moa_attn_num_splits(4, 8, 1024, 1024, 64, 64, 0) == 1      # short keys
+    # small prefill grids with long key ranges split the keys across workgroups:
+    # splits * (128-query tiles) approaches 256, with >= 1024 keys per split
+    assert moa.moa_attn_num_splits(1, 32, 128, 32768, 128, 128, 0) == 8
+    assert moa.moa_attn_num_splits(1, 2, 8192, 8192, 128, 128, 0) == 2
+    assert moa.moa_attn_num_splits(1, 1, 64, 4096, 64, 64, 0) == 4         # capped by Nk / 1024
+    ws = moa.moa_attn_workspace_bytes(1, 32, 128, 32768, 128, 128, 0)
+    assert ws == 32 * 128 * 8 * 130 * 4
+    # explicit prefill splits: 1 = one pass, more = that many
+    assert moa.moa_attn_num_splits(1, 32, 128, 32768, 128, 128, 1) == 1
+    assert moa.moa_attn_workspace_bytes(1, 32, 128, 32768, 128, 128, 1) == 0
+    assert moa.moa_attn_workspace_bytes(1, 1, 100, 300, 64, 64, 3) == -(-100 * 3 * 66 * 4 // 256) * 256
     # decode: partials of bh*splits rows of (d + 2) floats, rounded up to 256 B
     s = moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 0)
     assert 1 <= s <= 256
@@ -96,6 +109,9 @@ def _call(**kw):
     (dict(Nq=1), 3),                                   # decode needs a workspace
     (dict(Nq=1, workspace=W, workspace_bytes=16), 3),
     (dict(Nq=1, workspace=A, workspace_bytes=1 << 20), 1),   # workspace overlaps Q
+    (dict(num_splits=2), 3),                           # explicit prefill splits need a workspace
+    (dict(num_splits=2, workspace=W, workspace_bytes=256), 3),
+    (dict(num_splits=2, workspace=D, workspace_bytes=1 << 20), 1),   # workspace overlaps O
 ])
 def test_validation_rejects_before_any_gpu_work(kw, status):
     assert _call(**kw) == status
@@ -196,6 +212,8 @@ def test_empty_problems_are_no_ops():
     assert _call(B=0) == moa.MOA_OK
     assert _call(H=0) == moa.MOA_OK
     assert _call(Nq=0) == moa.MOA_OK
+    # fp32 prefill ignores a split request (it never splits), so an empty one is still OK
+    assert _call(B=0, in_dtype=moa.MOA_F32, out_dtype=moa.MOA_F32, num_splits=4) == moa.MOA_OK
 
 
 def test_one_hip_runtime_per_process():
