@@ -55,6 +55,10 @@ def _load():
         for f in (lib.oracle_attn_fwd, lib.oracle_attn_rows, lib.oracle_attn_weights,
                   lib.oracle_attn_bwd):
             f.restype = ci
+        lib.oracle_proj.argtypes = [vp, vp, ci, i64, i64, i64, i64, i64, vp, ci]
+        lib.oracle_proj.restype = ci
+        lib.oracle_bf16_round.argtypes = [vp, i64, vp]
+        lib.oracle_bf16_round.restype = None
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ci
         _lib = lib
@@ -145,6 +149,44 @@ def attention_bwd(q, k, v, do, scale=None, causal=False, nthreads=0):
     if rc != 0:
         raise ValueError(f"oracle_attn_bwd rejected the problem (code {rc})")
     return dq, dk_, dv_
+
+
+def projection(x, wt, H, d, nthreads=0):
+    """Exact fp64 projection in head-split form: x [B, N, Dm] and wt [H*d, Dm]
+    (fp32 or bf16 bit patterns) -> [B, H, N, d] with P[b,h,n,e] = sum_k x[b,n,k] wt[h*d+e, k]."""
+    x, wt = np.ascontiguousarray(x), np.ascontiguousarray(wt)
+    if x.dtype != wt.dtype or x.dtype not in (np.float32, np.uint16):
+        raise TypeError("x and wt share one storage type: float32 or bf16 bit patterns")
+    B, N, Dm = x.shape
+    if wt.shape != (H * d, Dm):
+        raise ValueError(f"wt must be [H*d, Dm] = {(H * d, Dm)}, got {wt.shape}")
+    p = np.empty((B, H, N, d), dtype=np.float64)
+    dt = F32 if x.dtype == np.float32 else BF16
+    rc = _load().oracle_proj(x.ctypes.data, wt.ctypes.data, dt, B, N, Dm, H, d, p.ctypes.data,
+                             int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle_proj rejected the problem")
+    return p
+
+
+def round_bf16(v):
+    """fp64 -> bf16 bit patterns (uint16), round to nearest even, directly from fp64."""
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = np.empty(v.shape, dtype=np.uint16)
+    _load().oracle_bf16_round(v.ctypes.data, v.size, out.ctypes.data)
+    return out
+
+
+def attention_proj(x, wq, wk, wv, H, d, scale=None, causal=False, nthreads=0, with_lse=False):
+    """Self-attention of a sequence through its input projections: Q, K, V = the exact
+    projections of x by wq, wk, wv (each [H*d, Dm]) rounded to bf16 -- the storage the
+    projected tensors have between the two steps -- then the attention oracle on them.
+    Returns (O, Q, K, V) with Q, K, V as bf16 bit patterns [B, H, N, d] (and LSE)."""
+    q, k, v = (round_bf16(projection(x, w, H, d, nthreads)) for w in (wq, wk, wv))
+    r = attention(q, k, v, scale=scale, causal=causal, nthreads=nthreads, with_lse=with_lse)
+    if with_lse:
+        return r[0], q, k, v, r[1]
+    return r, q, k, v
 
 
 def max_threads() -> int:

@@ -38,8 +38,9 @@
  *
  * Also returned on request: LSE[i] = m + ln(Z), the log of the softmax
  * denominator in natural-log units, and the full S and P matrices for tiny
- * shapes; and the backward pass (dQ, dK, dV for a given dO, see
- * oracle_attn_bwd below).
+ * shapes; the backward pass (dQ, dK, dV for a given dO, see oracle_attn_bwd
+ * below); and the input projections that produce Q, K and V from the
+ * sequence X (oracle_proj and oracle_bf16_round below).
  */
 #include <math.h>
 #include <stdint.h>
@@ -297,4 +298,61 @@ int oracle_max_threads(void) {
 #else
     return 1;
 #endif
+}
+
+/*
+ * Input projections (the paper's problem statement: Q = X W_Q, K = X W_K,
+ * V = X W_V).  X is [B][N][Dm] and each weight is given transposed, as
+ * Wt[f][k] = W[k][f] with f over the H*d projected features (the layout of a
+ * dense layer's weight); X and Wt are fp32 or bf16 bit patterns (same type).
+ * Writes the exact projection, in fp64, in head-split form:
+ *
+ *   P[b][h][n][e] = sum_{k=0}^{Dm-1} X[b][n][k] * Wt[h*d + e][k]
+ *
+ * summed in increasing k, with no reordering.  Returns 0, or -1 on invalid
+ * sizes.
+ */
+int oracle_proj(const void* X, const void* Wt, int dtype, int64_t B, int64_t N, int64_t Dm,
+                int64_t H, int64_t d, double* P, int nthreads) {
+    if (B < 0 || N < 0 || Dm < 1 || H < 0 || d < 1) return -1;
+    set_threads(nthreads);
+    const int64_t F = H * d;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < B * N; ++r) {
+        const int64_t b = r / N, n = r % N;
+        for (int64_t f = 0; f < F; ++f) {
+            double acc = 0.0;
+            for (int64_t k = 0; k < Dm; ++k)
+                acc += elem(X, dtype, r * Dm + k) * elem(Wt, dtype, f * Dm + k);
+            const int64_t h = f / d, e = f % d;
+            P[((b * H + h) * N + n) * d + e] = acc;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Round fp64 values to bf16, nearest with ties to even, directly from the fp64
+ * value (no intermediate fp32, so no double rounding): the significand is
+ * scaled to 8 bits and rounded by the FPU's default round-to-nearest-even.
+ * Normal range only (|v| in [2^-126, 2^128)) and zero; that covers every value
+ * the tests produce.  Writes bf16 bit patterns.
+ */
+void oracle_bf16_round(const double* v, int64_t n, uint16_t* out) {
+    for (int64_t i = 0; i < n; ++i) {
+        const double x = v[i];
+        double y = 0.0;
+        if (x != 0.0) {
+            int e;
+            const double m = frexp(fabs(x), &e);           /* |x| = m * 2^e, m in [0.5, 1) */
+            y = ldexp(nearbyint(ldexp(m, 8)), e - 8);      /* 8 significant bits */
+            if (x < 0) y = -y;
+        } else if (signbit(x)) {
+            y = -0.0;
+        }
+        const float f = (float)y;                          /* exact: 8 significant bits */
+        uint32_t bits;
+        memcpy(&bits, &f, sizeof bits);
+        out[i] = (uint16_t)(bits >> 16);
+    }
 }

@@ -353,3 +353,81 @@ def test_backward_rejects_bad_problems():
         oracle.attention_bwd(q, q, q, q[:, :, :3], causal=False)      # dO shape
     with pytest.raises(ValueError):
         oracle.attention_bwd(q, q[:, :, :3], q[:, :, :3], q, causal=True)   # causal Nq > Nk
+
+
+# ---------------------------------------------------------------- input projections
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 3, 8, 2, 4), (2, 5, 16, 3, 8), (1, 7, 64, 2, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_projection_matches_library_matmul(shape, dtype):
+    # The oracle's plain loops against numpy's matmul (a different implementation).
+    B, N, Dm, H, d = shape
+    x = synth.normal(920, (B, N, Dm), 1.0, dtype)
+    wt = synth.normal(921, (H * d, Dm), 0.5, dtype)
+    p = oracle.projection(x, wt, H, d)
+    xf = synth.bf16_bits_to_f32(x).astype(np.float64) if dtype == "bf16" else x.astype(np.float64)
+    wf = synth.bf16_bits_to_f32(wt).astype(np.float64) if dtype == "bf16" else wt.astype(np.float64)
+    ref = (xf @ wf.T).reshape(B, N, H, d).transpose(0, 2, 1, 3)
+    assert np.max(np.abs(p - ref)) <= 1e-12 * max(1.0, np.abs(ref).max())
+
+
+def test_projection_identity_weights_select_features():
+    # Wt = I (Dm = H*d): the head-split projection is X itself, regrouped by head.
+    B, N, H, d = 2, 3, 2, 4
+    x = synth.normal(922, (B, N, H * d), 1.0, "f32")
+    p = oracle.projection(x, np.eye(H * d, dtype=np.float32), H, d)
+    assert np.array_equal(p, x.astype(np.float64).reshape(B, N, H, d).transpose(0, 2, 1, 3))
+
+
+def _bf16_value(bits):
+    return synth.bf16_bits_to_f32(np.asarray(bits, dtype=np.uint16)).astype(np.float64)
+
+
+def test_bf16_rounding_is_nearest_even_from_fp64():
+    # Brute force: the result is the nearer of the two bf16 values bracketing v, and
+    # on an exact tie the one with an even last significand bit.
+    rng = np.random.default_rng(7)
+    v = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-6, 6, 4000),
+                        [0.0, -0.0, 1.0, -2.5, 3.0e30]])
+    # exact ties and near-ties: midpoints between neighbouring bf16 values, nudged
+    base = _bf16_value(rng.integers(0x3c00, 0x4400, 200))
+    mid = base * (1.0 + 2.0 ** -8)
+    v = np.concatenate([v, mid, np.nextafter(mid, np.inf), np.nextafter(mid, -np.inf)])
+    got = oracle.round_bf16(v)
+    f32 = v.astype(np.float32)
+    bits32 = f32.view(np.uint32)
+    lo_bits = (bits32 >> 16).astype(np.uint16)
+    for i, x in enumerate(v):
+        if x == 0.0:
+            assert _bf16_value(got[i]) == 0.0
+            continue
+        cands = [int(lo_bits[i]) + o for o in (-1, 0, 1, 2)]
+        vals = _bf16_value(cands)
+        dist = np.abs(vals - x)
+        best = dist.min()
+        winners = [c for c, dd in zip(cands, dist) if dd == best]
+        want = winners[0] if len(winners) == 1 else [c for c in winners if c % 2 == 0][0]
+        assert int(got[i]) == want, (x, got[i], want)
+
+
+def test_bf16_rounding_agrees_with_torch_on_fp32_values():
+    # For values that are already fp32 there is no double rounding, so torch's
+    # fp32 -> bf16 conversion is an independent reference.
+    import torch
+    x = synth.normal(923, (5000,), 3.0, "f32")
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(oracle.round_bf16(x.astype(np.float64)), ref)
+
+
+def test_attention_proj_composes_projection_rounding_and_attention():
+    B, N, Dm, H, d = 1, 6, 32, 2, 16
+    x = synth.normal(924, (B, N, Dm), 1.0, "bf16")
+    wq, wk, wv = (synth.normal(925 + i, (H * d, Dm), 0.2, "bf16") for i in range(3))
+    o, q, k, v = oracle.attention_proj(x, wq, wk, wv, H, d, causal=True)
+    assert np.array_equal(q, oracle.round_bf16(oracle.projection(x, wq, H, d)))
+    assert np.array_equal(o, oracle.attention(q, k, v, causal=True))
+    # A sequence of identical tokens gives identical V rows: every output row is that row.
+    x_same = np.repeat(x[:, :1, :], N, axis=1)
+    o2, _, _, v2 = oracle.attention_proj(x_same, wq, wk, wv, H, d, causal=True)
+    assert np.max(np.abs(o2 - _bf16_value(v2[:, :, :1, :]))) < 1e-12
