@@ -30,7 +30,7 @@
  *  - The library allocates no device memory, keeps no state between calls,
  *    never synchronises, and is safe to call from several host threads.  Work
  *    is enqueued on `stream` (at most two kernels for the forward, three for
- *    the backward); errors raised by kernels
+ *    the projected forward and for the backward); errors raised by kernels
  *    surface at the caller's next synchronisation.
  *  - Arguments are validated on the host before any HIP call; a rejected call
  *    touches no device memory.
@@ -233,6 +233,60 @@ int moa_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  int64_t Nk, int64_t dk, int64_t dv, float scale, int causal, int in_dtype,
                  int o_dtype, int grad_dtype, void* workspace, size_t workspace_bytes,
                  void* stream);
+
+/*
+ * moa_attn_proj_workspace_bytes -- device workspace a moa_attn_fwd_proj call
+ * with these dimensions needs, in bytes: the projected Q, K and V (bf16,
+ * B*H*N*d elements each, every one rounded up to 256 bytes) followed by the
+ * workspace moa_attn_fwd needs for the attention of those tensors.  0 for
+ * invalid or unsupported dimensions.
+ */
+size_t moa_attn_proj_workspace_bytes(int64_t B, int64_t N, int64_t Dm, int64_t H, int64_t d);
+
+/*
+ * moa_attn_fwd_proj -- self-attention of a sequence through its input
+ * projections: the paper's problem statement forms Q = X W_Q, K = X W_K,
+ * V = X W_V from the sequence X and then takes Attention(Q, K, V) (Sec. "MoA
+ * DNF Derivation of Attention", eq. attention), here for H heads of size d:
+ *
+ *   Q[b,h,n,e] = sum_k X[b,n,k] * W_Q[k, h*d + e]      (likewise K, V)
+ *   O[b,h,:,:] = attention of moa_attn_fwd on Q, K, V (Nq = Nk = N)
+ *
+ * X         device input, bf16 [B][N][Dm] (token rows, Dm contiguous).
+ * Wq, Wk, Wv
+ *           device inputs, bf16 [H*d][Dm]: each weight matrix TRANSPOSED,
+ *           Wq[f][k] = W_Q[k][f] (the row-major layout of a dense layer's
+ *           weight; the k index is contiguous, as in X).
+ * O, LSE    as for moa_attn_fwd, [B][H][N][d] (out_dtype MOA_F32 or
+ *           MOA_BF16) and optional fp32 [B][H][N].
+ * B, N, Dm, H, d
+ *           batch, tokens per sequence, model width, heads, head size.
+ *           Supported: d in {64, 128}, Dm a multiple of 64.
+ * scale, causal
+ *           as for moa_attn_fwd (Nq = Nk = N).
+ * workspace, workspace_bytes
+ *           device scratch of at least moa_attn_proj_workspace_bytes(...)
+ *           bytes, 16-byte aligned (required when B*H*N > 0).  On return the
+ *           projected Q, K, V sit at its start (bf16 [B][H][N][d] each, at
+ *           byte offsets 0, S and 2 S with S = B*H*N*d*2 rounded up to 256).
+ * stream    hipStream_t as void*.
+ *
+ * Computation: the three projections are one bf16 matrix-core product with
+ * fp32 accumulation, rounded to bf16 (nearest even) as they are stored; the
+ * attention then runs exactly as moa_attn_fwd on bf16 inputs.  Nothing but
+ * Q, K, V (and the attention's own partial states when it splits its keys)
+ * is written besides O and LSE.
+ *
+ * Buffers: O, LSE and the workspace must not overlap each other or X, Wq, Wk,
+ * Wv (else MOA_ERR_INVALID_ARG).  Pointers may be NULL only when B*H*N == 0
+ * (LSE: always).  Returns MOA_OK once the work is enqueued (or when
+ * B*H*N == 0: nothing is launched), else a MOA_ERR_* code; an unsupported d
+ * or Dm gives MOA_ERR_UNSUPPORTED.
+ */
+int moa_attn_fwd_proj(const void* X, const void* Wq, const void* Wk, const void* Wv, void* O,
+                      float* LSE, int64_t B, int64_t N, int64_t Dm, int64_t H, int64_t d,
+                      float scale, int causal, int out_dtype, void* workspace,
+                      size_t workspace_bytes, void* stream);
 
 /* moa_attn_status_string -- static, human-readable text for a status code. */
 const char* moa_attn_status_string(int status);

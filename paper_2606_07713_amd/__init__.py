@@ -3,7 +3,8 @@
 A thin binding over ``libmoa_attn.so``, whose C ABI is ``include/moa_attn.h``.
 The Python names mirror the C entry points (``moa_attn_fwd``,
 ``moa_attn_fwd_strided``, ``moa_attn_bwd``, ``moa_attn_workspace_bytes``,
-``moa_attn_bwd_workspace_bytes``, ``moa_attn_num_splits``,
+``moa_attn_bwd_workspace_bytes``, ``moa_attn_num_splits``, ``moa_attn_fwd_proj``,
+``moa_attn_proj_workspace_bytes``,
 ``moa_attn_status_string``) and only marshal arguments; every step of the
 computation runs in the library's HIP kernels.  ``attn_fwd`` is a convenience
 wrapper for torch tensors (torch supplies device memory and the stream).
@@ -22,7 +23,7 @@ __all__ = [
     "MOA_F32", "MOA_BF16", "MoaAttnError", "moa_attn_fwd", "moa_attn_workspace_bytes",
     "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd",
     "moa_attn_fwd_strided", "moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "attn_bwd", "LIB_PATH",
-    "lib",
+    "lib", "moa_attn_fwd_proj", "moa_attn_proj_workspace_bytes", "attn_fwd_proj",
 ]
 
 MOA_OK, MOA_ERR_INVALID_ARG, MOA_ERR_UNSUPPORTED, MOA_ERR_WORKSPACE, MOA_ERR_HIP = 0, 1, 2, 3, 4
@@ -61,6 +62,10 @@ lib.moa_attn_bwd_workspace_bytes.argtypes = [_i64] * 6
 lib.moa_attn_bwd_workspace_bytes.restype = _sz
 lib.moa_attn_bwd.argtypes = [_vp] * 9 + [_i64] * 6 + [_f32, _ci, _ci, _ci, _ci, _vp, _sz, _vp]
 lib.moa_attn_bwd.restype = _ci
+lib.moa_attn_proj_workspace_bytes.argtypes = [_i64] * 5
+lib.moa_attn_proj_workspace_bytes.restype = _sz
+lib.moa_attn_fwd_proj.argtypes = [_vp] * 6 + [_i64] * 5 + [_f32, _ci, _ci, _vp, _sz, _vp]
+lib.moa_attn_fwd_proj.restype = _ci
 lib.moa_attn_status_string.argtypes = [_ci]
 lib.moa_attn_status_string.restype = ctypes.c_char_p
 lib.moa_attn_last_hip_error.argtypes = []
@@ -240,3 +245,59 @@ def attn_bwd(q, k, v, o, lse, do, scale=None, causal=False, grad_dtype=None, wor
     if st != MOA_OK:
         raise MoaAttnError(st)
     return dq, dkk, dvv
+
+
+def moa_attn_proj_workspace_bytes(B, N, Dm, H, d) -> int:
+    return int(lib.moa_attn_proj_workspace_bytes(B, N, Dm, H, d))
+
+
+def moa_attn_fwd_proj(X, Wq, Wk, Wv, O, LSE, B, N, Dm, H, d, scale, causal, out_dtype, workspace,
+                      workspace_bytes, stream) -> int:
+    """Raw C call of the projected forward: pointers are ints (device addresses) or None;
+    returns the status."""
+    return int(lib.moa_attn_fwd_proj(X, Wq, Wk, Wv, O, LSE, B, N, Dm, H, d, float(scale),
+                                     int(causal), out_dtype, workspace, workspace_bytes, stream))
+
+
+def attn_fwd_proj(x, wq, wk, wv, heads, scale=None, causal=False, out_dtype=None,
+                  return_lse=False, return_qkv=False, workspace=None, stream=None):
+    """Self-attention of x [B, N, Dm] (bf16) through the input projections wq, wk, wv
+    ([H*d, Dm] bf16 each: the weights transposed, as a dense layer stores them) for
+    ``heads`` heads.  Returns O [B, H, N, d] (default dtype bf16), then LSE [B, H, N] when
+    ``return_lse``, then the projected (Q, K, V) [B, H, N, d] bf16 when ``return_qkv``.
+    ``scale`` defaults to 1/sqrt(d).  Raises ``MoaAttnError`` on a rejected call."""
+    import torch
+    for t in (x, wq, wk, wv):
+        if not t.is_cuda or not t.is_contiguous() or t.dtype != torch.bfloat16:
+            raise ValueError("x, wq, wk, wv must be contiguous bf16 device tensors")
+    B, N, Dm = x.shape
+    F = wq.shape[0]
+    if F % heads or tuple(wq.shape) != (F, Dm) or wk.shape != wq.shape or wv.shape != wq.shape:
+        raise ValueError("wq, wk, wv must all be [heads*d, Dm]")
+    d = F // heads
+    odt = torch.bfloat16 if out_dtype is None else out_dtype
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    out = torch.empty((B, heads, N, d), dtype=odt, device=x.device)
+    lse = torch.empty((B, heads, N), dtype=torch.float32, device=x.device) if return_lse else None
+    need = moa_attn_proj_workspace_bytes(B, N, Dm, heads, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    st = moa_attn_fwd_proj(x.data_ptr(), wq.data_ptr(), wk.data_ptr(), wv.data_ptr(),
+                           out.data_ptr(), lse.data_ptr() if lse is not None else None,
+                           B, N, Dm, heads, d, scale, causal, _dtype_code(odt),
+                           workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                           stream.cuda_stream)
+    if st != MOA_OK:
+        raise MoaAttnError(st)
+    res = [out]
+    if return_lse:
+        res.append(lse)
+    if return_qkv:
+        sz = -(-(B * heads * N * d * 2) // 256) * 256
+        raw = workspace.view(torch.uint8)
+        res.append(tuple(raw[i * sz: i * sz + B * heads * N * d * 2].view(torch.bfloat16)
+                         .view(B, heads, N, d) for i in range(3)))
+    return res[0] if len(res) == 1 else tuple(res)

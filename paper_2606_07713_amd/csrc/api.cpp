@@ -7,6 +7,7 @@
 
 #include "../../include/moa_attn.h"
 #include "launch.h"
+#include "proj.h"
 
 namespace {
 
@@ -358,6 +359,69 @@ int moa_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
         return MOA_ERR_HIP;
     }
     return MOA_OK;
+}
+
+size_t moa_attn_proj_workspace_bytes(int64_t B, int64_t N, int64_t Dm, int64_t H, int64_t d) {
+    if (B < 0 || N < 0 || Dm < 1 || H < 0 || !head_supported(d, d) || Dm % 64) return 0;
+    if (!sizes_fit(B, H, N, N, d)) return 0;
+    const size_t qkv = align256((size_t)(B * H * N * d) * 2);
+    const size_t att = N > 0 ? moa_attn_workspace_bytes(B, H, N, N, d, d, 0) : 0;
+    return 3 * qkv + att;
+}
+
+int moa_attn_fwd_proj(const void* X, const void* Wq, const void* Wk, const void* Wv, void* O,
+                      float* LSE, int64_t B, int64_t N, int64_t Dm, int64_t H, int64_t d,
+                      float scale, int causal, int out_dtype, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+    // ---- validation: no HIP call happens before all of it has passed
+    if (B < 0 || N < 0 || H < 0 || Dm < 1 || d < 1) return MOA_ERR_INVALID_ARG;
+    const int64_t bh = B * H, tokens = B * N;
+    const bool any = bh > 0 && N > 0;
+    if (any && (!X || !Wq || !Wk || !Wv || !O)) return MOA_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return MOA_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1) return MOA_ERR_INVALID_ARG;
+    if (out_dtype != MOA_F32 && out_dtype != MOA_BF16) return MOA_ERR_INVALID_ARG;
+    const void* ptrs[] = {X, Wq, Wk, Wv, O, LSE, workspace};
+    for (const void* q : ptrs)
+        if (!aligned16(q)) return MOA_ERR_INVALID_ARG;
+    if (!head_supported(d, d)) return MOA_ERR_UNSUPPORTED;
+    if (Dm % 64) return MOA_ERR_UNSUPPORTED;
+    if (!sizes_fit(B, H, N, N, d)) return MOA_ERR_UNSUPPORTED;
+    const int64_t lim = std::numeric_limits<int32_t>::max();
+    if (tokens > lim || H * d > lim / 3 || (tokens > 0 && Dm > lim / tokens)) return MOA_ERR_UNSUPPORTED;
+    if (!any) return MOA_OK;
+
+    const size_t need = moa_attn_proj_workspace_bytes(B, N, Dm, H, d);
+    if (!workspace || workspace_bytes < need) return MOA_ERR_WORKSPACE;
+    const size_t xn = (size_t)(tokens * Dm) * 2, wn = (size_t)(H * d * Dm) * 2;
+    const size_t on = (size_t)(bh * N * d) * (out_dtype == MOA_F32 ? 4 : 2);
+    const size_t ln = LSE ? (size_t)(bh * N) * sizeof(float) : 0;
+    struct Buf { const void* p; size_t n; };
+    const Buf ins[] = {{X, xn}, {Wq, wn}, {Wk, wn}, {Wv, wn}};
+    const Buf outs[] = {{O, on}, {LSE, ln}, {workspace, need}};
+    for (int i = 0; i < 3; ++i) {
+        for (const Buf& b : ins)
+            if (overlaps(outs[i].p, outs[i].n, b.p, b.n)) return MOA_ERR_INVALID_ARG;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return MOA_ERR_INVALID_ARG;
+    }
+
+    // Q, K, V (bf16, [B][H][N][d]) and the attention's own workspace.
+    const size_t qkv = align256((size_t)(bh * N * d) * 2);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    moa::ProjProblem pp;
+    pp.x = X;
+    pp.w[0] = Wq; pp.w[1] = Wk; pp.w[2] = Wv;
+    for (int i = 0; i < 3; ++i) pp.out[i] = ws + i * qkv;
+    pp.m = (int)tokens; pp.n = (int)N; pp.dm = (int)Dm; pp.h = (int)H; pp.d = (int)d;
+    const hipError_t e = moa::launch_proj(pp, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = hipGetErrorName(e);
+        return MOA_ERR_HIP;
+    }
+    return fwd_impl(pp.out[0], pp.out[1], pp.out[2], O, LSE, B, H, N, N, d, d, nullptr, nullptr,
+                    nullptr, nullptr, scale, causal, MOA_BF16, out_dtype, ws + 3 * qkv,
+                    need - 3 * qkv, 0, stream);
 }
 
 const char* moa_attn_last_hip_error(void) { return g_last_hip_error; }

@@ -21,7 +21,8 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = _declared_functions()
     assert names == ["moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "moa_attn_fwd",
-                     "moa_attn_fwd_strided", "moa_attn_last_hip_error", "moa_attn_num_splits",
+                     "moa_attn_fwd_proj", "moa_attn_fwd_strided", "moa_attn_last_hip_error",
+                     "moa_attn_num_splits", "moa_attn_proj_workspace_bytes",
                      "moa_attn_status_string", "moa_attn_workspace_bytes"]
 
 
@@ -227,3 +228,47 @@ def test_one_hip_runtime_per_process():
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip().splitlines()[-1] == "1"
+
+
+X_, WQ, WK, WV = 11 << 40, 12 << 40, 13 << 40, 14 << 40
+
+
+def _call_proj(**kw):
+    args = dict(X=X_, Wq=WQ, Wk=WK, Wv=WV, O=D, LSE=None, B=2, N=16, Dm=128, H=2, d=64,
+                scale=0.125, causal=0, out_dtype=moa.MOA_BF16, workspace=W,
+                workspace_bytes=1 << 30, stream=None)
+    args.update(kw)
+    return moa.moa_attn_fwd_proj(**args)
+
+
+def test_proj_workspace_bytes():
+    # Q, K, V in bf16, each rounded up to 256 bytes, then the attention's own workspace
+    qkv = 2 * 2 * 16 * 64 * 2
+    assert moa.moa_attn_proj_workspace_bytes(2, 16, 128, 2, 64) == 3 * qkv
+    # one token per sequence: the attention is decode-shaped and needs its partials
+    one = moa.moa_attn_proj_workspace_bytes(4, 1, 128, 2, 128)
+    assert one == 3 * 2048 + moa.moa_attn_workspace_bytes(4, 2, 1, 1, 128, 128, 0)
+    # a small grid with a long sequence: split-K partials are included
+    long_ = moa.moa_attn_proj_workspace_bytes(1, 8192, 512, 2, 128)
+    assert long_ == 3 * 2 * 8192 * 128 * 2 + moa.moa_attn_workspace_bytes(1, 2, 8192, 8192, 128, 128, 0)
+    assert moa.moa_attn_proj_workspace_bytes(1, 16, 100, 2, 64) == 0      # Dm not a multiple of 64
+    assert moa.moa_attn_proj_workspace_bytes(1, 16, 128, 2, 96) == 0      # unsupported head
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(X=None), 1), (dict(Wk=None), 1), (dict(O=None), 1),
+    (dict(B=-1), 1), (dict(Dm=0), 1), (dict(scale=float("inf")), 1), (dict(causal=2), 1),
+    (dict(out_dtype=3), 1), (dict(X=X_ + 8), 1), (dict(LSE=L + 4), 1),
+    (dict(O=X_ + 64), 1),                              # O overlaps X
+    (dict(workspace=WV + 256), 1),                     # workspace overlaps Wv
+    (dict(LSE=W + 1024), 1),                           # LSE inside the workspace
+    (dict(d=96), 2), (dict(Dm=96), 2),
+    (dict(workspace=None), 3), (dict(workspace_bytes=1024), 3),
+])
+def test_proj_validation_rejects_before_any_gpu_work(kw, status):
+    assert _call_proj(**kw) == status
+
+
+def test_proj_empty_problems_are_no_ops():
+    assert _call_proj(B=0) == moa.MOA_OK
+    assert _call_proj(N=0, X=None, O=None, workspace=None) == moa.MOA_OK
