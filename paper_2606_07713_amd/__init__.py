@@ -185,6 +185,8 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
                          "dimension is contiguous")
     lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device) if return_lse else None
     ws_bytes = moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits)
+    if in_code == MOA_F32 and Nq != 1:
+        ws_bytes = 0          # fp32 prefill never splits its keys
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     if stream is None:
