@@ -18,13 +18,17 @@
 //    rows as A operands, Q and dO fragments held in registers as in the
 //    forward), dS^T in registers, dQ^T += K^T dS^T with K^T from transposing
 //    LDS reads of the same K stage.
-//  * bwd_dkdv: one item = 128 keys of one (b, h); Q, dO, LSE and D stream
-//    through LDS in 64-query stages.  S = Q K^T and dP = dO V^T (Q and dO rows
-//    as A operands, K and V fragments in registers), so a lane holds one key;
-//    dV^T += dO^T P and dK^T += Q^T dS with dO^T and Q^T from transposing
-//    reads.  Every lane owns its key's rows of dK and dV: no atomics, and the
-//    results are deterministic.
-// P and dS are rounded to bf16 for the matrix products (fp32 accumulation).
+//  * bwd_dkdv_pair: one item = 128 keys of one (b, h); Q, dO, LSE and D
+//    stream through LDS in 64-query stages.  S = Q K^T and dP = dO V^T (Q and
+//    dO rows as A operands, K or V fragments in registers), so a lane holds
+//    one key; dV^T += dO^T P and dK^T += Q^T dS with dO^T and Q^T from
+//    transposing reads.  The two halves of that work go to two waves of the
+//    same SIMD (the weights P pass between them through LDS), so the vector
+//    work of one overlaps the matrix products of the other.  Every lane owns
+//    its key's rows of dK or dV: no atomics, and the results are
+//    deterministic.
+// P and dS are rounded to bf16 for the matrix products (fp32 accumulation);
+// dS is formed from the bf16-rounded P.
 #include <algorithm>
 #include <type_traits>
 
@@ -131,33 +135,63 @@ __device__ __forceinline__ void pack16(const float (&x)[16], bf16x8 (&pb)[2]) {
     }
 }
 
-// Register-staged stage loads: the i-th 16-byte load of lane l of wave w
-// reads chunk S = (w*LPS + i)*64 + l of the stage (coalesced) and stores it
-// at LDS row S / CHUNKS, physical chunk (S % CHUNKS) ^ swz(row).
+// A direct-to-LDS 16-byte load (buffer_load_dwordx4 ... lds) as inline
+// assembly, invisible to the compiler's wait-count tracking (whose aliasing
+// model cannot tell the slots of one LDS ring apart and would wait for every
+// load before any read of the ring).  The
+// caller waits for it itself (s_waitcnt vmcnt, then a barrier) before any wave
+// reads the data; loads complete in issue order, so the compiler's own waits
+// for later loads stay correct.  `rsrc` holds the four descriptor words (see
+// rsrc_words), `lds_addr` the wave-uniform LDS byte address.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, bytes, 0x00020000u};
+}
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+    return (uint32_t)reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p);
+}
+// M0 is listed as clobbered: clang warns that it does not preserve reserved
+// registers around the statement; the kernels of this file set M0 nowhere
+// else (their assembly has no other M0 write).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void buffer_load16_to_lds_untracked(u32x4 rsrc, uint32_t lds_addr, uint32_t voffset) {
+    const u32x4 r = {(uint32_t)__builtin_amdgcn_readfirstlane(rsrc[0]), (uint32_t)__builtin_amdgcn_readfirstlane(rsrc[1]),
+                     (uint32_t)__builtin_amdgcn_readfirstlane(rsrc[2]), (uint32_t)__builtin_amdgcn_readfirstlane(rsrc[3])};
+    const uint32_t m = (uint32_t)__builtin_amdgcn_readfirstlane(lds_addr);
+    // One wait state between the M0 write and the load that reads it.
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(m), "v"(voffset), "s"(r) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Direct-to-LDS stage loads (untracked: the caller waits with vmcnt and a
+// barrier): lane l of the i-th load of wave w fills slot S = (w*LPS + i)*64
+// + l of the stage, which holds logical chunk (S % CHUNKS) ^ swz(row) of row
+// S / CHUNKS (the forward's swizzled layout).
 template <int D, int NW>
-struct Stager {
+struct DmaStager {
     static constexpr int LPS = Cfg<D>::TILE_BYTES / (NW * 1024);
     static_assert(Cfg<D>::TILE_BYTES % (NW * 1024) == 0, "a stage must split into wave loads");
-    uint32_t goff[LPS], woff[LPS];
-    __device__ __forceinline__ Stager(int wave, int lane) {
+    uint32_t goff[LPS];
+    uint32_t lds_off;        // this wave's first 1 KB of a stage
+    __device__ __forceinline__ DmaStager(int wave, int lane) {
+        lds_off = (uint32_t)wave * LPS * 1024u;
 #pragma unroll
         for (int i = 0; i < LPS; ++i) {
             const int slot = (wave * LPS + i) * 64 + lane;
             const int row = slot / Cfg<D>::CHUNKS, p = slot % Cfg<D>::CHUNKS;
-            goff[i] = (uint32_t)slot * 16u;
-            woff[i] = (uint32_t)row * Cfg<D>::ROW_BYTES + (uint32_t)((p ^ swz<D>(row)) * 16);
+            goff[i] = (uint32_t)row * Cfg<D>::ROW_BYTES + (uint32_t)((p ^ swz<D>(row)) * 16);
         }
     }
-    // Rows j*64 .. j*64 + 63 of a head slice of `n` rows; rows past n are zero.
-    __device__ __forceinline__ void load(const u16* head, int n, int j, uint4 (&st)[LPS]) const {
+    // Rows j*64 .. j*64 + 63 of a head slice of `n` rows into `stage`; rows
+    // past n are zero.
+    __device__ __forceinline__ void issue(const u16* head, int n, int j, unsigned char* stage) const {
         const int r0 = min(j * BN, n);
-        const auto r = make_rsrc(head + (size_t)r0 * D, (uint32_t)(n - r0) * Cfg<D>::ROW_BYTES);
+        const u32x4 r = rsrc_words(head + (size_t)r0 * D, (uint32_t)(n - r0) * Cfg<D>::ROW_BYTES);
+        const uint32_t base = lds_address(stage) + lds_off;
 #pragma unroll
-        for (int i = 0; i < LPS; ++i) st[i] = buffer_load16(r, goff[i]);
-    }
-    __device__ __forceinline__ void store(unsigned char* slot, const uint4 (&st)[LPS]) const {
-#pragma unroll
-        for (int i = 0; i < LPS; ++i) *reinterpret_cast<uint4*>(slot + woff[i]) = st[i];
+        for (int i = 0; i < LPS; ++i) buffer_load16_to_lds_untracked(r, base + i * 1024u, goff[i]);
     }
 };
 
@@ -198,12 +232,12 @@ __global__ __launch_bounds__(DQ_THREADS, 1) void bwd_dq_kernel(
     __shared__ __attribute__((aligned(1024))) unsigned char v_r0[C::TILE_BYTES];
     __shared__ __attribute__((aligned(1024))) unsigned char v_r1[C::TILE_BYTES];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 31, half = lane >> 5;
     const int off = Nk - Nq;
     const TileAddr<D> ta(lane);
-    const Stager<D, DQ_WAVES> stg(wave, lane);
-    using Stage = uint4[Stager<D, DQ_WAVES>::LPS];
+    const DmaStager<D, DQ_WAVES> stg(wave, lane);
 
     for (int item = 0;; ++item) {
         int bh, qt;
@@ -271,19 +305,22 @@ __global__ __launch_bounds__(DQ_THREADS, 1) void bwd_dq_kernel(
                                                                      acc[b], 0, 0, 0);
         };
 
-        // Stage iteration j: K(j), V(j) in slot j & 1; K(j+1), V(j+1) in flight.
-        Stage sk, sv;
-        stg.load(Kh, Nk, 0, sk);
-        stg.load(Vh, Nk, 0, sv);
+        // Stage iteration j: K(j), V(j) in slot j & 1.  Right after the
+        // barrier the loads of K(j+1), V(j+1) start into the other slot,
+        // whose readers (iteration j - 1) are done; each wave waits for its
+        // own loads before the next barrier.
+        stg.issue(Kh, Nk, 0, k_r0);
+        stg.issue(Vh, Nk, 0, v_r0);
         for (int j = 0; j < n_stages; ++j) {
             unsigned char* ks = (j & 1) ? k_r1 : k_r0;
             unsigned char* vs = (j & 1) ? v_r1 : v_r0;
-            stg.store(ks, sk);
-            stg.store(vs, sv);
-            stg.load(Kh, Nk, j + 1, sk);
-            stg.load(Vh, Nk, j + 1, sv);
+            wait_vmcnt<0>();
             wait_lgkmcnt0();
             barrier_no_fence();
+            if (j + 1 < n_stages) {
+                stg.issue(Kh, Nk, j + 1, (j & 1) ? k_r0 : k_r1);
+                stg.issue(Vh, Nk, j + 1, (j & 1) ? v_r0 : v_r1);
+            }
             if (2 * j < n_w) step(ks, vs, 0, 2 * j);
             if (2 * j + 1 < n_w) step(ks, vs, 1, 2 * j + 1);
         }
@@ -293,32 +330,40 @@ __global__ __launch_bounds__(DQ_THREADS, 1) void bwd_dq_kernel(
     }
 }
 
-// ---- dK, dV: 4 waves x 32 keys (one wave per SIMD: the four accumulators
-// and K, V fragments need more than 256 registers); Q / dO stages of 64.
-constexpr int KV_WAVES = 4;
-constexpr int KV_THREADS = KV_WAVES * 64;
-constexpr int KV_BN = KV_WAVES * 32;
+// ---- dK, dV with two waves per SIMD: 8 waves, 128 keys per item.  Wave w
+// < 4 (role A) owns keys 32w .. 32w + 31 of the item for dV: S = Q K^T, the
+// weights P (exponentials), dV^T += dO^T P, and P handed to its partner
+// through LDS as bf16.  Wave w + 4 (role B, on the same SIMD) owns the same
+// keys for dK: dP = dO V^T, dS = P (dP - D) with the partner's P, dK^T +=
+// Q^T dS.  The matrix work of a step splits evenly between the two waves and
+// nothing is computed twice; B runs one 64-query stage behind A, so the LDS
+// ring holds three Q / dO stages and two stages of exchanged weights.
+constexpr int KV2_WAVES = 8;
+constexpr int KV2_THREADS = KV2_WAVES * 64;
+constexpr int KV2_BN = 4 * 32;   // keys per item
+constexpr int KV2_RING = 3;      // Q / dO stages in LDS
 
 template <int D, bool CAUSAL, bool OUT_BF16>
-__global__ __launch_bounds__(KV_THREADS, 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(KV2_THREADS, 1) void bwd_dkdv_pair_kernel(
     const u16* __restrict__ Q, const u16* __restrict__ K, const u16* __restrict__ V,
     const u16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Dsum,
     void* __restrict__ dK, void* __restrict__ dV, int Nq, int Nk, int n_bh, int n_ktiles, float c,
     float scale) {
     using C = Cfg<D>;
     constexpr uint32_t RB = C::ROW_BYTES;
-    __shared__ __attribute__((aligned(1024))) unsigned char q_r0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char q_r1[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char g_r0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(1024))) unsigned char g_r1[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(16))) float l_r[2][2][BN];   // [slot][lse2, D][query]
+    __shared__ __attribute__((aligned(1024))) unsigned char q_r[KV2_RING][C::TILE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char g_r[KV2_RING][C::TILE_BYTES];
+    // Exchanged weights: [stage parity][key block][32-query half][chunk c2][lane] x 16 bytes.
+    __shared__ __attribute__((aligned(1024))) uint4 p_x[2][4][2][2][64];
+    __shared__ __attribute__((aligned(16))) float l_r[KV2_RING][2][BN];   // [slot][lse2, D][query]
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int role = wave >> 2, kb = wave & 3;   // role 0: P and dV; role 1: dS and dK
     const int col = lane & 31, half = lane >> 5;
     const int off = Nk - Nq;
     const TileAddr<D> ta(lane);
-    const Stager<D, KV_WAVES> stg(wave, lane);
-    using Stage = uint4[Stager<D, KV_WAVES>::LPS];
+    const DmaStager<D, KV2_WAVES> stg(wave, lane);
 
     for (int item = 0;; ++item) {
         int bh, rt;
@@ -326,120 +371,158 @@ __global__ __launch_bounds__(KV_THREADS, 1) void bwd_dkdv_kernel(
         // Causal key tiles cost most at the start of the sequence: the
         // heaviest-first rank order of item_of is reversed here.
         const int kt = CAUSAL ? n_ktiles - 1 - rt : rt;
-        const int k0 = kt * KV_BN;
-        const int krow = k0 + wave * 32 + col;
+        const int k0 = kt * KV2_BN;
+        const int krow = k0 + kb * 32 + col;
         const bool key_ok = krow < Nk;
         const u16* Qh = Q + (size_t)bh * Nq * D;
         const u16* Gh = dO + (size_t)bh * Nq * D;
         const float* Lh = LSE + (size_t)bh * Nq;
         const float* Dh = Dsum + (size_t)bh * Nq;
 
-        // K and V fragments of this lane's key (B operands).
-        bf16x8 kf[D / 16], vf[D / 16];
+        // K (role A) or V (role B) fragment of this lane's key: B operands.
+        bf16x8 kvf[D / 16];
         {
-            const auto rk = make_rsrc(K + (size_t)bh * Nk * D, (uint32_t)Nk * RB);
-            const auto rv = make_rsrc(V + (size_t)bh * Nk * D, (uint32_t)Nk * RB);
+            const auto r = make_rsrc((role == 0 ? K : V) + (size_t)bh * Nk * D, (uint32_t)Nk * RB);
 #pragma unroll
-            for (int s = 0; s < D / 16; ++s) {
-                kf[s] = __builtin_bit_cast(bf16x8, buffer_load16(rk, (uint32_t)krow * RB + s * 32 + half * 16));
-                vf[s] = __builtin_bit_cast(bf16x8, buffer_load16(rv, (uint32_t)krow * RB + s * 32 + half * 16));
-            }
+            for (int s = 0; s < D / 16; ++s)
+                kvf[s] = __builtin_bit_cast(bf16x8, buffer_load16(r, (uint32_t)krow * RB + s * 32 + half * 16));
         }
 
         // Queries that see any key of the tile (query i sees key j iff
-        // j <= i + off), in 64-query stages; this wave's first needed step.
+        // j <= i + off), in 64-query stages; the block's first needed step.
         const int q_lo = CAUSAL ? max(0, k0 - off) : 0;
         const int st0 = q_lo / BN;
         const int n_stages = (Nq + BN - 1) / BN - st0;
-        const int wave_k_first = k0 + wave * 32;
-        const int t_first = CAUSAL ? max(0, wave_k_first - off) / SUB : 0;   // global 32-query step
-        const bool wave_live = wave_k_first < Nk;
+        const int blk_k_first = k0 + kb * 32;
+        const int t_first = CAUSAL ? max(0, blk_k_first - off) / SUB : 0;   // global 32-query step
+        const bool blk_live = blk_k_first < Nk;
 
-        f32x16 dk[D / 32], dv[D / 32];
+        f32x16 acc[D / 32];          // dV^T (role A) or dK^T (role B)
 #pragma unroll
-        for (int b = 0; b < D / 32; ++b) { dk[b] = f32x16{}; dv[b] = f32x16{}; }
+        for (int b = 0; b < D / 32; ++b) acc[b] = f32x16{};
 
-        auto step = [&](const unsigned char* qs, const unsigned char* gs, const float* ls, const float* dsv,
-                        int u, int t) __attribute__((always_inline)) {
-            f32x16 s = f32x16{}, dp = f32x16{};
+        // Role A, step u of stage js: weights of 32 queries x this lane's key.
+        auto step_a = [&](const unsigned char* qs, const unsigned char* gs, const float* ls, uint4* px,
+                          int u, int t) __attribute__((always_inline)) {
+            f32x16 s = f32x16{};
 #pragma unroll
-            for (int k = 0; k < D / 16; ++k) {
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_rows<D>(qs, ta, u, k), kf[k], s, 0, 0, 0);
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_rows<D>(gs, ta, u, k), vf[k], dp, 0, 0, 0);
-            }
+            for (int k = 0; k < D / 16; ++k)
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_rows<D>(qs, ta, u, k), kvf[k], s, 0, 0, 0);
             const int qbase = t * SUB;
-            const bool need_mask = (qbase + SUB > Nq) || (CAUSAL && qbase < wave_k_first + 31 - off);
-            float p[16], ds[16];
+            const bool need_mask = (qbase + SUB > Nq) || (CAUSAL && qbase < blk_k_first + 31 - off);
+            float p[16];
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int m0 = 32 * u + 8 * g + 4 * half;   // stage-local query of element 4g
                 const float4 l4 = *reinterpret_cast<const float4*>(ls + m0);
-                const float4 d4 = *reinterpret_cast<const float4*>(dsv + m0);
-                const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+                const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int i = 4 * g + r;
-                    float t = __builtin_fmaf(s[i], c, -lv[r]);
+                    float x = __builtin_fmaf(s[i], c, -lv[r]);
                     if (need_mask) {
                         const int qi = qbase + 8 * g + 4 * half + r;
-                        if (qi >= Nq || (CAUSAL && krow > qi + off)) t = kNegInf;
+                        if (qi >= Nq || (CAUSAL && krow > qi + off)) x = kNegInf;
                     }
-                    p[i] = exp2_hw(t);
-                    ds[i] = p[i] * (dp[i] - dvv[r]);
+                    p[i] = exp2_hw(x);
                 }
             }
-            bf16x8 pb[2], dsb[2];
+            bf16x8 pb[2];
             pack16(p, pb);
+#pragma unroll
+            for (int c2 = 0; c2 < 2; ++c2) px[c2 * 64 + lane] = __builtin_bit_cast(uint4, pb[c2]);
+#pragma unroll
+            for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+                for (int b = 0; b < D / 32; ++b)
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_tr<D>(gs, ta, b, 2 * u + c2), pb[c2],
+                                                                     acc[b], 0, 0, 0);
+        };
+
+        // Role B, step u of stage js: dS from the partner's weights.
+        auto step_b = [&](const unsigned char* qs, const unsigned char* gs, const float* dsv, const uint4* px,
+                          int u) __attribute__((always_inline)) {
+            f32x16 dp = f32x16{};
+#pragma unroll
+            for (int k = 0; k < D / 16; ++k)
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_rows<D>(gs, ta, u, k), kvf[k], dp, 0, 0, 0);
+            const uint4 w0 = px[lane], w1 = px[64 + lane];
+            const uint32_t pw[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            float ds[16];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int m0 = 32 * u + 8 * g + 4 * half;
+                const float4 d4 = *reinterpret_cast<const float4*>(dsv + m0);
+                const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = 4 * g + r;
+                    const float pi = (i & 1) ? bf16hi_to_f32(pw[i >> 1]) : bf16lo_to_f32(pw[i >> 1]);
+                    ds[i] = pi * (dp[i] - dvv[r]);
+                }
+            }
+            bf16x8 dsb[2];
             pack16(ds, dsb);
 #pragma unroll
             for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-                for (int b = 0; b < D / 32; ++b) {
-                    dv[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_tr<D>(gs, ta, b, 2 * u + c2), pb[c2],
-                                                                    dv[b], 0, 0, 0);
-                    dk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_tr<D>(qs, ta, b, 2 * u + c2), dsb[c2],
-                                                                    dk[b], 0, 0, 0);
-                }
+                for (int b = 0; b < D / 32; ++b)
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(stage_tr<D>(qs, ta, b, 2 * u + c2), dsb[c2],
+                                                                     acc[b], 0, 0, 0);
         };
 
-        // LSE and D of a stage's 64 queries: one float per lane of wave 0
-        // and wave 1 (zero past Nq).  The value is used one stage later, so
-        // the load stays in flight with the Q and dO loads.
+        // LSE and D of a stage's 64 queries: one float per lane of waves 0
+        // and 1 (zero past Nq), stored one iteration after the load.
         auto load_ld = [&](int js, float& x) __attribute__((always_inline)) {
             const int qi = js * BN + lane;
             x = 0.0f;
             if (wave < 2 && qi < Nq) x = (wave == 0) ? Lh[qi] : Dh[qi];
         };
 
-        Stage sq, sg;
+        // Iteration j: stage st0 + j is in the ring; role A works on it,
+        // role B on the stage before (whose weights A wrote in iteration
+        // j - 1).  Right after the barrier the loads of stage j + 1 start
+        // into the slot whose last reader (role B, iteration j - 1) is done,
+        // and each wave waits for its own loads before the next barrier.
         float sx;
-        stg.load(Qh, Nq, st0, sq);
-        stg.load(Gh, Nq, st0, sg);
+        stg.issue(Qh, Nq, st0, q_r[0]);
+        stg.issue(Gh, Nq, st0, g_r[0]);
         load_ld(st0, sx);
-        for (int j = 0; j < n_stages; ++j) {
+        for (int j = 0; j <= n_stages; ++j) {
             const int js = st0 + j;
-            const int slot = j & 1;
-            unsigned char* qs = slot ? q_r1 : q_r0;
-            unsigned char* gs = slot ? g_r1 : g_r0;
-            stg.store(qs, sq);
-            stg.store(gs, sg);
-            if (wave < 2) l_r[slot][wave][lane] = (wave == 0) ? sx * kLog2e : sx;
-            stg.load(Qh, Nq, js + 1, sq);
-            stg.load(Gh, Nq, js + 1, sg);
-            load_ld(js + 1, sx);
+            const int slot = j % KV2_RING;
+            if (j < n_stages && wave < 2) l_r[slot][wave][lane] = (wave == 0) ? sx * kLog2e : sx;
+            wait_vmcnt<0>();
             wait_lgkmcnt0();
             barrier_no_fence();
-            if (wave_live) {
-                if (2 * js >= t_first) step(qs, gs, l_r[slot][0], l_r[slot][1], 0, 2 * js);
-                if (2 * js + 1 >= t_first) step(qs, gs, l_r[slot][0], l_r[slot][1], 1, 2 * js + 1);
+            if (j + 1 < n_stages) {
+                const int ns = (j + 1) % KV2_RING;
+                stg.issue(Qh, Nq, js + 1, q_r[ns]);
+                stg.issue(Gh, Nq, js + 1, g_r[ns]);
+                load_ld(js + 1, sx);
+            }
+            if (!blk_live) continue;
+            if (role == 0) {
+                if (j < n_stages) {
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+                        if (2 * js + u >= t_first)
+                            step_a(q_r[slot], g_r[slot], l_r[slot][0], &p_x[j & 1][kb][u][0][0], u, 2 * js + u);
+                }
+            } else if (j >= 1) {
+                const int ps = (j - 1) % KV2_RING;
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    if (2 * (js - 1) + u >= t_first)
+                        step_b(q_r[ps], g_r[ps], l_r[ps][1], &p_x[(j - 1) & 1][kb][u][0][0], u);
             }
         }
         wait_lgkmcnt0();
         barrier_no_fence();
         if (key_ok) {
             const size_t base = ((size_t)bh * Nk + krow) * D;
-            store_rows16<D, OUT_BF16>(dK, base, half, dk, scale);
-            store_rows16<D, OUT_BF16>(dV, base, half, dv, 1.0f);
+            if (role == 0) store_rows16<D, OUT_BF16>(dV, base, half, acc, 1.0f);
+            else store_rows16<D, OUT_BF16>(dK, base, half, acc, scale);
         }
     }
 }
@@ -481,12 +564,12 @@ hipError_t launch(const BwdProblem& p, hipStream_t stream) {
     }
     // dK, dV (zero when there are no queries)
     {
-        auto kernel = bwd_dkdv_kernel<D, CAUSAL, OUT_BF16>;
-        static const int per_cu = resident_per_cu(kernel, KV_THREADS);
-        const int n_kt = (p.nk + KV_BN - 1) / KV_BN;
+        auto kernel = bwd_dkdv_pair_kernel<D, CAUSAL, OUT_BF16>;
+        static const int per_cu = resident_per_cu(kernel, KV2_THREADS);
+        const int n_kt = (p.nk + KV2_BN - 1) / KV2_BN;
         const long long items = (long long)p.bh * n_kt;
         const unsigned grid = (unsigned)std::min<long long>(items, (long long)cus * per_cu);
-        e = launch_kernel(kernel, dim3(grid), dim3(KV_THREADS), stream, static_cast<const u16*>(p.q),
+        e = launch_kernel(kernel, dim3(grid), dim3(KV2_THREADS), stream, static_cast<const u16*>(p.q),
                           static_cast<const u16*>(p.k), static_cast<const u16*>(p.v),
                           static_cast<const u16*>(p.dout), p.lse, static_cast<const float*>(p.dsum),
                           p.dk, p.dv, p.nq, p.nk, p.bh, n_kt, c, p.scale);
