@@ -66,6 +66,9 @@ SHAPES = [
     (2, 100, 64, 1, 64),       # ragged tokens; 3*H*d = 192: a partial feature tile
     (3, 77, 320, 3, 128),      # batches straddle token tiles
     (1, 300, 256, 4, 64),
+    # H*d a multiple of 256: the one-projection-per-tile kernel
+    (3, 77, 320, 2, 128),      # three feature tiles, batches straddle a ragged token tile
+    (2, 300, 192, 4, 128),     # two feature tiles per projection, odd k-step count
 ]
 
 
