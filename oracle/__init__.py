@@ -52,8 +52,10 @@ def _load():
         lib.oracle_attn_rows.argtypes = [vp, vp, vp, ci] + dims + [f32, ci, vp, i64, vp, vp, ci]
         lib.oracle_attn_weights.argtypes = [vp, vp, vp, ci] + dims + [f32, ci, vp, vp, vp, vp]
         lib.oracle_attn_bwd.argtypes = [vp, vp, vp, vp, ci] + dims + [f32, ci, vp, vp, vp, ci]
+        lib.oracle_attn_bwd_rows.argtypes = ([vp, vp, vp, vp, ci] + dims +
+                                             [f32, ci, i64, vp, i64, vp, i64, vp, vp, vp, ci])
         for f in (lib.oracle_attn_fwd, lib.oracle_attn_rows, lib.oracle_attn_weights,
-                  lib.oracle_attn_bwd):
+                  lib.oracle_attn_bwd, lib.oracle_attn_bwd_rows):
             f.restype = ci
         lib.oracle_proj.argtypes = [vp, vp, ci, i64, i64, i64, i64, i64, vp, ci]
         lib.oracle_proj.restype = ci
@@ -148,6 +150,29 @@ def attention_bwd(q, k, v, do, scale=None, causal=False, nthreads=0):
                                  dq.ctypes.data, dk_.ctypes.data, dv_.ctypes.data, int(nthreads))
     if rc != 0:
         raise ValueError(f"oracle_attn_bwd rejected the problem (code {rc})")
+    return dq, dk_, dv_
+
+
+def attention_bwd_rows(q, k, v, do, bh, qrows, krows, scale=None, causal=False, nthreads=0):
+    """The gradients of ``attention_bwd`` at sampled outputs of head slice ``bh`` (b*H + h):
+    dQ [len(qrows), dk] at query rows ``qrows`` and dK, dV [len(krows), .] at key rows
+    ``krows`` (indices within the slice), fp64."""
+    q, k, v, dt, (B, H, Nq, Nk, dk, dv) = _prep(q, k, v)
+    do = np.ascontiguousarray(do)
+    if do.dtype != q.dtype or do.shape != (B, H, Nq, dv):
+        raise ValueError("dO must have the storage type of Q and shape [B, H, Nq, dv]")
+    qrows = np.ascontiguousarray(qrows, dtype=np.int64)
+    krows = np.ascontiguousarray(krows, dtype=np.int64)
+    dq = np.empty((qrows.size, dk), dtype=np.float64)
+    dk_ = np.empty((krows.size, dk), dtype=np.float64)
+    dv_ = np.empty((krows.size, dv), dtype=np.float64)
+    rc = _load().oracle_attn_bwd_rows(q.ctypes.data, k.ctypes.data, v.ctypes.data, do.ctypes.data,
+                                      dt, B, H, Nq, Nk, dk, dv, _scale(scale, dk),
+                                      int(bool(causal)), int(bh), qrows.ctypes.data, qrows.size,
+                                      krows.ctypes.data, krows.size, dq.ctypes.data,
+                                      dk_.ctypes.data, dv_.ctypes.data, int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_attn_bwd_rows rejected the problem (code {rc})")
     return dq, dk_, dv_
 
 

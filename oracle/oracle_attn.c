@@ -291,6 +291,117 @@ int oracle_attn_bwd(const void* Q, const void* K, const void* V, const void* dO,
     return 0;
 }
 
+/*
+ * The same gradients at sampled outputs of one head slice bh (0 <= bh < B*H):
+ * dQ at the query rows qrows[0..nq) and dK, dV at the key rows krows[0..nk)
+ * of that slice (row indices within the slice).  Long sequences need this:
+ * the full pass above costs O(Nq * Nk * d) per head with no shortcut.
+ *
+ * Every query row i of the slice first goes through attend_row (Steps I-IV,
+ * its weights w[k] and output row O_i).  With dP_ik = <dO_i, V_k>:
+ *   D_i  = sum_c dO_i[c] * O_i[c]      (= sum_k w_ik dP_ik, by the definition
+ *                                        of O_i; taken in this form here so
+ *                                        that a row needs dP only at the
+ *                                        sampled keys)
+ *   dS_ik = w_ik * (dP_ik - D_i)
+ *   dQ_i  = scale * sum_k dS_ik K_k      (sampled i, all k, increasing k)
+ *   dK_k  = scale * sum_i dS_ik Q_i      (sampled k, all i, increasing i)
+ *   dV_k  =         sum_i w_ik dO_i      (sampled k, all i, increasing i)
+ * Returns 0, 1 on invalid arguments, 2 when scratch memory is short.
+ */
+int oracle_attn_bwd_rows(const void* Q, const void* K, const void* V, const void* dO, int dtype,
+                         int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                         float scale, int causal, int64_t bh, const int64_t* qrows, int64_t nq,
+                         const int64_t* krows, int64_t nk, double* dQ, double* dK, double* dV,
+                         int nthreads) {
+    problem_t p = {Q, K, V, dtype, B, H, Nq, Nk, dk, dv, (double)scale, causal};
+    if (check(&p) || !dO || bh < 0 || bh >= B * H || nq < 0 || nk < 0) return 1;
+    if ((nq && (!qrows || !dQ)) || (nk && (!krows || !dK || !dV))) return 1;
+    for (int64_t x = 0; x < nq; ++x)
+        if (qrows[x] < 0 || qrows[x] >= Nq) return 1;
+    for (int64_t x = 0; x < nk; ++x)
+        if (krows[x] < 0 || krows[x] >= Nk) return 1;
+    set_threads(nthreads);
+    int nt = 1;
+#ifdef _OPENMP
+    nt = omp_get_max_threads();
+#endif
+    const size_t per = 3 * (size_t)Nk + (size_t)dv;
+    double* scratch = (double*)malloc((size_t)nt * per * sizeof(double));
+    /* per query row and sampled key: the weight w_ik and dS_ik */
+    double* wk = (double*)malloc(((size_t)Nq * (size_t)(nk ? nk : 1)) * sizeof(double));
+    double* sk = (double*)malloc(((size_t)Nq * (size_t)(nk ? nk : 1)) * sizeof(double));
+    if (!scratch || !wk || !sk) {
+        free(scratch); free(wk); free(sk);
+        return 2;
+    }
+    const int64_t k_base = bh * Nk * dk, v_base = bh * Nk * dv;
+#pragma omp parallel num_threads(nt)
+    {
+        int tid = 0;
+#ifdef _OPENMP
+        tid = omp_get_thread_num();
+#endif
+        double* s = scratch + (size_t)tid * per;
+        double* e = s + Nk;
+        double* w = e + Nk;
+        double* o_row = w + Nk;
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t i = 0; i < Nq; ++i) {
+            const int64_t r = bh * Nq + i;
+            attend_row(&p, r, s, e, w, o_row, NULL, NULL, NULL);
+            const int64_t q_row = r * dk, o_off = r * dv;
+            double D = 0.0;
+            for (int64_t c = 0; c < dv; ++c) D += elem(dO, dtype, o_off + c) * o_row[c];
+            for (int64_t x = 0; x < nk; ++x) {
+                const int64_t k = krows[x];
+                double ds = 0.0;
+                if (s[k] != -INFINITY) {
+                    double dp = 0.0;
+                    for (int64_t c = 0; c < dv; ++c)
+                        dp += elem(dO, dtype, o_off + c) * elem(V, dtype, v_base + k * dv + c);
+                    ds = w[k] * (dp - D);
+                }
+                wk[(size_t)i * nk + x] = w[k];
+                sk[(size_t)i * nk + x] = ds;
+            }
+            for (int64_t y = 0; y < nq; ++y) {
+                if (qrows[y] != i) continue;
+                double* dq_row = dQ + y * dk;
+                for (int64_t j = 0; j < dk; ++j) dq_row[j] = 0.0;
+                for (int64_t k = 0; k < Nk; ++k) {
+                    if (s[k] == -INFINITY) continue;
+                    double dp = 0.0;
+                    for (int64_t c = 0; c < dv; ++c)
+                        dp += elem(dO, dtype, o_off + c) * elem(V, dtype, v_base + k * dv + c);
+                    const double ds = w[k] * (dp - D);
+                    for (int64_t j = 0; j < dk; ++j)
+                        dq_row[j] += (double)scale * ds * elem(K, dtype, k_base + k * dk + j);
+                }
+            }
+            (void)q_row;
+        }
+#pragma omp for schedule(static)
+        for (int64_t x = 0; x < nk; ++x) {
+            double* dk_row = dK + x * dk;
+            double* dv_row = dV + x * dv;
+            for (int64_t j = 0; j < dk; ++j) dk_row[j] = 0.0;
+            for (int64_t c = 0; c < dv; ++c) dv_row[c] = 0.0;
+            for (int64_t i = 0; i < Nq; ++i) {
+                const double wi = wk[(size_t)i * nk + x], ds = sk[(size_t)i * nk + x];
+                if (wi == 0.0 && ds == 0.0) continue;
+                const int64_t q_row = (bh * Nq + i) * dk, o_off = (bh * Nq + i) * dv;
+                for (int64_t j = 0; j < dk; ++j) dk_row[j] += (double)scale * ds * elem(Q, dtype, q_row + j);
+                for (int64_t c = 0; c < dv; ++c) dv_row[c] += wi * elem(dO, dtype, o_off + c);
+            }
+        }
+    }
+    free(scratch);
+    free(wk);
+    free(sk);
+    return 0;
+}
+
 /* Threads OpenMP would use for a call with nthreads <= 0. */
 int oracle_max_threads(void) {
 #ifdef _OPENMP

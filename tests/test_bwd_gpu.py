@@ -195,3 +195,65 @@ def test_bwd_without_queries_zeroes_key_gradients():
     torch.cuda.synchronize()
     assert dq.numel() == 0
     assert torch.count_nonzero(dk).item() == 0 and torch.count_nonzero(dv).item() == 0
+
+
+def _bounds_rows(q, k, v, do, bh, qrows, krows, scale, causal, chunk=1024):
+    """The tolerance scales of _bounds at sampled rows of head slice bh, in query chunks
+    (no Nq x Nk matrix is held)."""
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    b, h = divmod(bh, H)
+    Q, K, V, G = (_f64(a[b, h]) for a in (q, k, v, do))
+    Ka, Va, Ga, Qa = np.abs(K), np.abs(V), np.abs(G), np.abs(Q)
+    s = abs(float(np.float32(scale)))
+    off = Nk - Nq
+    bq = np.zeros((len(qrows), d))
+    bk = np.zeros((len(krows), d))
+    bv = np.zeros((len(krows), d))
+    qpos = {int(i): n for n, i in enumerate(qrows)}
+    for i0 in range(0, Nq, chunk):
+        i1 = min(Nq, i0 + chunk)
+        S = float(np.float32(scale)) * (Q[i0:i1] @ K.T)
+        if causal:
+            S[np.arange(Nk)[None, :] > (np.arange(i0, i1)[:, None] + off)] = -np.inf
+        P = np.exp(S - S.max(axis=1, keepdims=True))
+        P /= P.sum(axis=1, keepdims=True)
+        dabs = np.sum((P @ Va) * Ga[i0:i1], axis=1)                 # sum_j P_ij A_ij
+        Pk = P[:, krows]
+        Ak = Ga[i0:i1] @ Va[krows].T
+        bk += s * ((Pk * (Ak + dabs[:, None])).T @ Qa[i0:i1])
+        bv += Pk.T @ Ga[i0:i1]
+        for i in range(i0, i1):
+            if i in qpos:
+                a_row = Ga[i] @ Va.T
+                bq[qpos[i]] = s * ((P[i - i0] * (a_row + dabs[i - i0])) @ Ka)
+    return bq, bk, bv
+
+
+def test_bwd_full_size_sampled():
+    """The 16K causal workload at full size (B1 H32 d128, logits of sigma 3), as bench.py runs
+    it: O and LSE from this library's forward, fp32 gradients; sampled rows of two heads
+    (tile edges of both gradient kernels, the first and last rows) against the oracle."""
+    import torch
+    import paper_2606_07713_amd as moa
+    w = synth.WORKLOADS["causal_long_b1h32_n16384_d128_bf16_qk_sigma3"]
+    q, k, v = synth.make_inputs(w)
+    do = synth.normal(7919, (w.B, w.H, w.Nq, w.dv), 1.0, "bf16")
+    say("bwd full size: GPU forward and backward")
+    tq, tk, tv, tg = (synth.to_torch(a, "cuda") for a in (q, k, v, do))
+    o, lse = moa.attn_fwd(tq, tk, tv, scale=w.scale, causal=True, out_dtype=torch.float32,
+                          return_lse=True)
+    dq, dk, dv = moa.attn_bwd(tq, tk, tv, o, lse, tg, scale=w.scale, causal=True,
+                              grad_dtype=torch.float32)
+    torch.cuda.synchronize()
+    qrows = np.array([0, 1, 31, 32, 255, 256, 4095, 8191, 8192, 12345, 16383])
+    krows = np.array([0, 1, 127, 128, 129, 4096, 8000, 16255, 16256, 16383])
+    for bh in (0, w.H - 1):
+        b, h = divmod(bh, w.H)
+        say(f" head {bh}: oracle on {qrows.size} query and {krows.size} key rows")
+        ref = oracle.attention_bwd_rows(q, k, v, do, bh, qrows, krows, scale=w.scale, causal=True)
+        got = (dq[b, h][torch.from_numpy(qrows).cuda()].double().cpu().numpy(),
+               dk[b, h][torch.from_numpy(krows).cuda()].double().cpu().numpy(),
+               dv[b, h][torch.from_numpy(krows).cuda()].double().cpu().numpy())
+        bounds = _bounds_rows(q, k, v, do, bh, qrows, krows, w.scale, True)
+        _check(got, ref, bounds, TOL_END_TO_END)

@@ -355,6 +355,40 @@ def test_backward_rejects_bad_problems():
         oracle.attention_bwd(q, q[:, :, :3], q[:, :, :3], q, causal=True)   # causal Nq > Nk
 
 
+@pytest.mark.parametrize("shape", [(1, 2, 9, 13, 16, 16), (2, 1, 40, 40, 32, 8), (1, 1, 3, 70, 64, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_backward_rows_match_torch_autograd_fp64(shape, causal):
+    """The sampled-rows backward (used at sequence lengths the full pass cannot reach) gives
+    torch autograd's fp64 gradients at its rows, for every head slice, edge rows included."""
+    B, H, Nq, Nk, dk, dv = shape
+    q = synth.normal(941, (B, H, Nq, dk), 1.0, "bf16")
+    k = synth.normal(942, (B, H, Nk, dk), 1.0, "bf16")
+    v = synth.normal(943, (B, H, Nk, dv), 1.0, "bf16")
+    do = synth.normal(944, (B, H, Nq, dv), 1.0, "bf16")
+    scale = float(np.float32(1 / np.sqrt(dk)))
+    rq, rk, rv = _torch_grads(q, k, v, do, scale, causal)
+    qrows = np.array(sorted({0, Nq // 2, Nq - 1}))
+    krows = np.array(sorted({0, 1, Nk // 3, Nk - 1}))
+    for bh in range(B * H):
+        b, h = divmod(bh, H)
+        dq, dk_, dv_ = oracle.attention_bwd_rows(q, k, v, do, bh, qrows, krows, scale=scale,
+                                                 causal=causal)
+        assert np.max(np.abs(dq - rq[b, h, qrows])) < 1e-12
+        assert np.max(np.abs(dk_ - rk[b, h, krows])) < 1e-12
+        assert np.max(np.abs(dv_ - rv[b, h, krows])) < 1e-12
+
+
+def test_backward_rows_rejects_bad_rows():
+    q = synth.normal(950, (1, 2, 4, 8), 1.0, "f32")
+    with pytest.raises(ValueError):
+        oracle.attention_bwd_rows(q, q, q, q, 2, [0], [0])            # head slice past B*H
+    with pytest.raises(ValueError):
+        oracle.attention_bwd_rows(q, q, q, q, 0, [4], [0])            # query row past Nq
+    with pytest.raises(ValueError):
+        oracle.attention_bwd_rows(q, q, q, q, 0, [0], [-1])           # key row below 0
+
+
 # ---------------------------------------------------------------- input projections
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
