@@ -114,3 +114,38 @@ def test_projected_forward_long_sequence_splits_keys():
     err = max_err(o, ref_o)
     say(f"  max err {err:.3e}")
     assert err <= TOL["bf16"]
+
+
+def test_projected_forward_full_size_sampled():
+    """A model-sized call (B1 N4096 Dm4096 H32 d128, causal: 412 GFLOP of projections, the
+    first shape of the projection measurements): every projected element of one head at
+    sampled tokens, and sampled rows of that head's O and LSE, against the oracle (exact
+    projections of the head, rounded to bf16, then its attention)."""
+    import torch
+    import paper_2606_07713_amd as moa
+    B, N, Dm, H, d = 1, 4096, 4096, 32, 128
+    x, ws = _inputs(B, N, Dm, H, d, _seed("full"))
+    say("proj full size: GPU")
+    tx, tq, tk, tv = (synth.to_torch(a, "cuda") for a in (x, *ws))
+    o, lse, qkv = moa.attn_fwd_proj(tx, tq, tk, tv, H, causal=True, out_dtype=torch.float32,
+                                    return_lse=True, return_qkv=True)
+    torch.cuda.synchronize()
+    h = 19
+    toks = np.array([0, 1, 255, 256, 257, 1023, 2048, 3000, 4094, 4095])
+    hs = slice(h * d, (h + 1) * d)
+    say(f" head {h}: oracle projections of the head")
+    exact = [oracle.projection(x, w[hs], 1, d) for w in ws]          # [1, 1, N, d] each
+    for t, want, w in zip(qkv, exact, ws):
+        got = t[0, h].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)[toks]
+        frac = _check_projection(got[None, None], oracle.round_bf16(want[:, :, toks]),
+                                 x[:, toks], w[hs], 1, d)
+        assert frac < 0.01
+    rq, rk, rv = (oracle.round_bf16(a) for a in exact)
+    say(" oracle attention rows")
+    ref_o, ref_lse = oracle.attention_rows(rq, rk, rv, toks, causal=True, with_lse=True)
+    got_o = o[0, h].cpu().double().numpy()[toks]
+    got_lse = lse[0, h].cpu().double().numpy()[toks]
+    err = max_err(got_o, ref_o)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL["bf16"]
+    assert max_err(got_lse, ref_lse) <= 4e-3 + 1e-5 * np.abs(ref_lse).max()
