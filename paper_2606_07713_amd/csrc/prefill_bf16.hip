@@ -318,7 +318,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             // A row may have seen no visible key yet (its reference is still
             // -inf): there is nothing to rescale, and 2^(-inf - -inf) must
             // not be formed.
-            const float m_new = fmaxf(m_run, mt);
+            const float m_new = fmaxf(m_run, mt + kRefHeadroom);
             const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
             l_run *= alpha;
             alpha_pend = rescale_pend ? alpha_pend * alpha : alpha;
@@ -336,8 +336,9 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // reference without computing the tile max; only if a partial sum exceeds
     // kFastSumLimit (or overflowed) is the reference raised and the tile
     // redone.  Any reference gives the same quotient, so this is exact.  A
-    // row that has seen no key yet starts from its tile max instead (a guessed
-    // reference far above its scores would underflow every weight); rows
+    // row that has seen no key yet starts from its tile max plus
+    // kRefHeadroom instead (a guessed reference far above its scores would
+    // underflow every weight); rows
     // still without a visible key take reference 0, all their scores being
     // -inf.  The pass loop
     // is not unrolled so that pbuf has a single producer.

@@ -267,7 +267,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[i]);
             const float mt = half_max(mx) * c;
             if (wave_any(mt > m_run + kRescaleSlack)) {
-                const float m_new = fmaxf(m_run, mt);
+                const float m_new = fmaxf(m_run, mt + kRefHeadroom);
                 const float alpha = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - m_new);
                 l_run *= alpha;
                 alpha_pend = rescale_pend ? alpha_pend * alpha : alpha;
@@ -285,8 +285,9 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
         // the step max; only if a partial sum exceeds kFastSumLimit (or
         // overflowed) is the reference raised and the step redone.  Any
         // reference gives the same quotient, so this is exact.  A row that
-        // has seen no key yet starts from its step max instead (a guessed
-        // reference far above its scores would underflow every weight); rows
+        // has seen no key yet starts from its step max plus kRefHeadroom
+        // instead (a guessed reference far above its scores would underflow
+        // every weight); rows
         // still without a visible key take reference 0, all their scores
         // being -inf.
         auto softmax_pre = [&](f32x16& s, int t) __attribute__((always_inline)) {
