@@ -17,13 +17,13 @@ constexpr int THREADS = WAVES * 64;
 constexpr int BN = 64;                       // key rows per LDS tile
 constexpr float kRescaleSlack = 8.0f;        // log2 units a tile may exceed the reference by
 // A raised reference is set this far (log2 units) above the tile max that
-// raised it.  Weights then start at most 2^-16, which costs no precision (bf16
-// and fp32 share the exponent range; only keys ~110 units below the max would
+// raised it.  Weights then start at most 2^-32, which costs no precision (bf16
+// and fp32 share the exponent range; only keys ~94 units below the max would
 // flush to zero, far below fp32 resolution of the sum), and later tiles must
 // exceed the new reference by the fast-step limit before it is raised again:
 // with wide logits the first tiles' max is typically tens of units below the
 // row max, and each raise costs a redone tile.
-constexpr float kRefHeadroom = 16.0f;
+constexpr float kRefHeadroom = 32.0f;
 constexpr float kFastSumLimit = 1048576.0f;  // 2^20: partial sum bound of the fast step
 
 typedef short v4s __attribute__((ext_vector_type(4)));
