@@ -164,6 +164,44 @@ def test_unusual_scales(scale, dtype, nq):
     assert max_err(o, ref) <= TOL[dtype]
 
 
+# Key-split (4 items), per-wave pipelined (512 items) and ping-pong (1024 items)
+# layouts; the two larger ones are checked on sampled rows.
+EXTREME_SHAPES = [
+    # B, H, Nq, Nk, d
+    (2, 2, 77, 700, 128),
+    (1, 2, 300, 300, 64),
+    (2, 64, 1000, 1000, 64),
+    (4, 64, 1000, 1000, 64),
+]
+
+
+@pytest.mark.parametrize("scale", [4.0, 16.0])
+@pytest.mark.parametrize("shape", EXTREME_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_extreme_logit_spread(scale, shape, causal):
+    # Logits with a standard deviation of 45 to 260 log2 units per row: the
+    # running reference is raised again and again (each raise set well above
+    # the tile max that caused it), most weights underflow, and the result is
+    # close to a one-hot pick of each row's top keys.  bf16 inputs: the path
+    # whose softmax keeps the lazily raised reference.
+    B, H, Nq, Nk, d = shape
+    say(f"extreme logits scale={scale} {shape} causal={causal}")
+    q, k, v = gen(B, H, Nq, Nk, d, "bf16", seed=4242 + Nq + H)
+    o, lse = run_gpu(q, k, v, causal=causal, scale=scale, out_dtype="f32", return_lse=True)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    if B * H * Nq <= 1024:
+        ref, ref_lse = oracle_full(q, k, v, causal=causal, scale=scale, with_lse=True)
+    else:
+        rows = sample_rows(B, H, Nq, 256, seed=11, tile=256)
+        ref, ref_lse = oracle.attention_rows(q, k, v, rows, scale=scale, causal=causal,
+                                             with_lse=True)
+        o, lse = o.reshape(-1, d)[rows], lse.reshape(-1)[rows]
+    err = max_err(o, ref)
+    say(f"  max err {err:.3e}")
+    assert err <= TOL["bf16"]
+    assert max_err(lse, ref_lse) <= _lse_tol("bf16", ref_lse)
+
+
 # -------------------------------------------------------- full-size workloads
 
 def _check_workload(name, n_rows, out_dtype):
