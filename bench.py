@@ -15,10 +15,13 @@ MI355X peaks.  The fp64 CPU oracle is timed on a bounded sample of the
 prefill workload on the host's cores as a reported baseline.
 
 The backward pass of the prefill workload (dQ, dK, dV from the forward's O and
-LSE for a seeded dO) is timed in the same run and reported under "backward".
+LSE for a seeded dO) is timed in the same run and reported under "backward",
+and every one of the library's five workloads is timed and reported under
+"configs" (time, TFLOP/s and GB/s against the roofline that bounds it).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline] [--no-decode] [--no-backward] [--calibrate-copy MIB]
+                       [--no-cpu-baseline] [--no-decode] [--no-backward] [--no-configs]
+                       [--calibrate-copy MIB]
 """
 from __future__ import annotations
 
@@ -98,6 +101,28 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+def config_record(w, ms: float, out_bytes: int, layout: str = "bhnd") -> dict:
+    """Time and roofline figures of one workload: algorithmic flops and compulsory bytes per
+    call over the measured time, against the bf16 matrix-core and HBM peaks.  The fp32 path
+    (vector ALU, far below either roofline at its 4 MFLOP size) reports absolute time only."""
+    flops = algorithmic_flops(w)
+    nbytes = compulsory_bytes(w, out_bytes)
+    tflops = flops / (ms * 1e-3) / 1e12
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    rec = {"workload": w.name, "ms_per_call": round(ms, 5), "tflops": round(tflops, 2),
+           "GBps": round(gbs, 1), "flop_per_call": flops, "compulsory_bytes": nbytes,
+           "out": "bf16" if out_bytes == 2 else "f32"}
+    if w.dtype != "bf16":
+        rec.update(bound="latency", frac=None, traffic=None)
+    elif flops / nbytes > PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        rec.update(bound="mfma", frac=round(tflops / PEAK_BF16_TFLOPS, 4),
+                   traffic=measured_traffic("prefill_bf16", w.name) if layout == "bhnd" else None)
+    else:
+        rec.update(bound="hbm", frac=round(gbs / PEAK_HBM_GBS, 4),
+                   traffic=measured_traffic("decode_split", w.name) if layout == "bhnd" else None)
+    return rec
+
+
 def _inputs(w, dev):
     import synth
     q, k, v = synth.make_inputs(w)
@@ -165,6 +190,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the timing of the backward pass (reported under \"backward\")")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload records (reported under \"configs\")")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain copy kernel of MIB MiB (read MIB, "
                          "write MIB) so profiler byte counters can be scaled against it")
@@ -199,7 +226,7 @@ def main(argv=None):
         torch.cuda.synchronize()
         del src, dst
 
-    def run_workload(name):
+    def run_workload(name, steps=None):
         w = synth.WORKLOADS[name]
         host, (tq, tk, tv) = _inputs(w, dev)
         odt = {"bf16": torch.bfloat16, "f32": torch.float32}[args.out_dtype or w.dtype]
@@ -214,7 +241,7 @@ def main(argv=None):
         def call():
             moa.attn_fwd(tq, tk, tv, scale=w.scale, causal=w.causal, out_dtype=odt, out=out,
                          workspace=ws if ws_bytes else None, stream=stream)
-        ms = time_calls(call, args.steps, args.warmup, stream)
+        ms = time_calls(call, steps or args.steps, args.warmup, stream)
         return w, host, ms, out.element_size()
 
     w, host, ms, ob = run_workload(args.workload)
@@ -291,6 +318,23 @@ def main(argv=None):
         print(f"# backward {w.name}: {msb:.4f} ms/call, {fb / (msb * 1e-3) / 1e12:.1f} TFLOP/s",
               file=sys.stderr, flush=True)
         del o, lse, do, ws_bwd
+
+    if not args.no_configs:
+        # Every workload of the library, each timed like the main line (one library call per
+        # step, HIP events on the launch stream); the main and decode workloads reuse the
+        # timings above.
+        timed = {w.name: (ms, ob)}
+        if "decode" in line:
+            timed[wd.name] = (msd, obd)
+        recs = []
+        for name, wc in synth.WORKLOADS.items():
+            if name in timed:
+                msc, obc = timed[name]
+            else:
+                _, _, msc, obc = run_workload(name, max(args.steps, 100))
+            recs.append(config_record(wc, msc, obc, args.layout))
+            print(f"# config {name}: {msc * 1e3:.2f} us/call", file=sys.stderr, flush=True)
+        line["configs"] = recs
 
     line["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(w, host)
     print(json.dumps(line), flush=True)

@@ -49,3 +49,15 @@ def test_backward_flops_are_two_and_a_half_forwards():
     for name in ("causal_long_b1h32_n16384_d128_bf16_qk_sigma3", "mha_b4h8_n1024_d64_bf16"):
         w = synth.WORKLOADS[name]
         assert bench.backward_flops(w) == 2.5 * bench.algorithmic_flops(w)
+
+
+def test_config_records():
+    ws = synth.WORKLOADS
+    r = bench.config_record(ws["causal_b2h16_n4096_d128_bf16"], 0.1, 2)
+    assert r["bound"] == "mfma" and r["out"] == "bf16"
+    assert r["tflops"] == round(bench.algorithmic_flops(ws["causal_b2h16_n4096_d128_bf16"]) / 1e-4 / 1e12, 2)
+    assert r["frac"] == round(r["tflops"] / bench.PEAK_BF16_TFLOPS, 4)
+    r = bench.config_record(ws["decode_b64h32_nk8192_d128_bf16"], 1.0, 2)
+    assert r["bound"] == "hbm" and abs(r["frac"] - r["GBps"] / bench.PEAK_HBM_GBS) < 1e-4
+    r = bench.config_record(ws["single_head_f32_n128_d64"], 0.02, 4)
+    assert r["bound"] == "latency" and r["frac"] is None

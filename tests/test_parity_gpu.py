@@ -1,10 +1,13 @@
 """Parity of the HIP path with the fp64 oracle on the same seeded inputs.
 
 Tolerances (max-abs, relative to std(V) = 1): 1e-5 for fp32 inputs, 2e-2 for
-bf16 inputs.  Small and ragged shapes are compared element by element; the
-full-size workloads run in the launch configuration the benchmark times and
-are checked on sampled rows the oracle computes one by one.
+bf16 inputs.  Small and ragged shapes and the five full-size workloads are
+compared element by element (the workloads in the launch configuration the
+benchmark times); large layout-coverage shapes are checked on sampled rows the
+oracle computes one by one.
 """
+import os
+import time
 import zlib
 
 import numpy as np
@@ -203,46 +206,157 @@ def test_extreme_logit_spread(scale, shape, causal):
 
 
 # -------------------------------------------------------- full-size workloads
+#
+# Every output element of every workload is compared with the oracle, in the
+# launch configuration bench.py times (the library's own choice of layout and
+# splits).  The oracle of a workload is computed once per session and serves
+# both output storage types; the long causal workload takes about 40 s of host
+# time on 16 threads.
 
-def _check_workload(name, n_rows, out_dtype):
-    w = synth.WORKLOADS[name]
-    say(f"workload {name} -> {out_dtype}: generating inputs")
-    q, k, v = synth.make_inputs(w)
-    say("  running GPU")
-    o = run_gpu(q, k, v, causal=w.causal, scale=w.scale, out_dtype=out_dtype)
+_REF_CACHE = {}
+
+
+def _workload_ref(name):
+    if name not in _REF_CACHE:
+        _REF_CACHE.clear()          # one workload's arrays at a time
+        w = synth.WORKLOADS[name]
+        say(f"workload {name}: generating inputs")
+        q, k, v = synth.make_inputs(w)
+        threads = len(os.sched_getaffinity(0))
+        say(f"  oracle, all {w.B * w.H * w.Nq} rows, {threads} threads")
+        # One batch entry and a few heads per oracle call, so progress is visible.
+        ref = np.empty((w.B, w.H, w.Nq, w.dv))
+        ref_lse = np.empty((w.B, w.H, w.Nq))
+        hs = max(1, min(w.H, (1 << 22) // max(1, w.Nq * w.Nk // (2 if w.causal else 1) // 64)))
+        t0 = time.perf_counter()
+        for b in range(w.B):
+            for h0 in range(0, w.H, hs):
+                h1 = min(w.H, h0 + hs)
+                sl = (slice(b, b + 1), slice(h0, h1))
+                o, l = oracle.attention(*(np.ascontiguousarray(a[sl]) for a in (q, k, v)),
+                                        scale=w.scale, causal=w.causal, with_lse=True,
+                                        nthreads=threads)
+                ref[sl], ref_lse[sl] = o, l
+                if w.Nq * w.Nk >= 1 << 24:
+                    say(f"    batch {b} heads {h0}..{h1 - 1}: {time.perf_counter() - t0:.1f} s")
+        _REF_CACHE[name] = (w, (q, k, v), ref, ref_lse)
+    return _REF_CACHE[name]
+
+
+def _check_workload(name, out_dtype):
+    w, (q, k, v), ref, ref_lse = _workload_ref(name)
+    say(f"workload {name} -> {out_dtype}: running GPU")
+    o, lse = run_gpu(q, k, v, causal=w.causal, scale=w.scale, out_dtype=out_dtype,
+                     return_lse=True)
     assert np.all(np.isfinite(o))
-    if n_rows is None:
-        say("  oracle (all rows)")
-        ref = oracle.attention(q, k, v, scale=w.scale, causal=w.causal)
-        err = max_err(o, ref)
-    else:
-        rows = sample_rows(w.B, w.H, w.Nq, n_rows)
-        say(f"  oracle ({rows.size} sampled rows)")
-        ref = oracle.attention_rows(q, k, v, rows, scale=w.scale, causal=w.causal)
-        err = max_err(o.reshape(-1, w.dv)[rows], ref)
-    say(f"  max err {err:.3e}")
+    err = max_err(o, ref)
+    lse_err = max_err(lse, ref_lse)
+    say(f"  max |O - oracle| over all {o.size} outputs: {err:.3e}; max |LSE - oracle| {lse_err:.3e}")
     assert err <= TOL[w.dtype] * w.sigma_v
+    assert lse_err <= _lse_tol(w.dtype, ref_lse)
 
 
 def test_workload_single_head_f32():
-    _check_workload("single_head_f32_n128_d64", None, "f32")
+    _check_workload("single_head_f32_n128_d64", "f32")
 
 
 @pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
 def test_workload_mha_d64(out_dtype):
-    _check_workload("mha_b4h8_n1024_d64_bf16", None, out_dtype)
+    _check_workload("mha_b4h8_n1024_d64_bf16", out_dtype)
 
 
 @pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
 def test_workload_causal_4k(out_dtype):
-    _check_workload("causal_b2h16_n4096_d128_bf16", 384, out_dtype)
+    _check_workload("causal_b2h16_n4096_d128_bf16", out_dtype)
 
 
 @pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
 def test_workload_causal_16k_wide_logits(out_dtype):
-    _check_workload("causal_long_b1h32_n16384_d128_bf16_qk_sigma3", 192, out_dtype)
+    _check_workload("causal_long_b1h32_n16384_d128_bf16_qk_sigma3", out_dtype)
 
 
 @pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
 def test_workload_decode(out_dtype):
-    _check_workload("decode_b64h32_nk8192_d128_bf16", 512, out_dtype)
+    _check_workload("decode_b64h32_nk8192_d128_bf16", out_dtype)
+
+
+# ------------------------------------------------ brute force on tiny shapes
+
+TINY_N = (1, 2, 3, 5, 8, 17)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_shape_grid(d, causal, dtype):
+    # Every Nq, Nk in {1, 2, 3, 5, 8, 17} (causal: Nq <= Nk), two heads of two
+    # batches, every element against the oracle; O in the input type and in
+    # fp32.  Nq = 1 is the decode path, the rest prefill.
+    worst = 0.0
+    bad = []
+    for nq in TINY_N:
+        for nk in TINY_N:
+            if causal and nq > nk:
+                continue
+            q, k, v = gen(2, 2, nq, nk, d, dtype, seed=_seed("tiny", nq, nk, d, causal, dtype))
+            ref, ref_lse = oracle_full(q, k, v, causal=causal, with_lse=True)
+            for od in sorted({dtype, "f32"}):
+                o, lse = run_gpu(q, k, v, causal=causal, out_dtype=od, return_lse=True)
+                err = max_err(o, ref)
+                worst = max(worst, err)
+                if not (err <= TOL[dtype] and max_err(lse, ref_lse) <= _lse_tol(dtype, ref_lse)):
+                    bad.append((nq, nk, od, err, max_err(lse, ref_lse)))
+    say(f"tiny grid d={d} causal={causal} {dtype}: worst err {worst:.3e}")
+    assert not bad, bad
+
+
+# ------------------------------------- the paper's worked example on the GPU
+
+def test_worked_example_through_the_library(golden_dir):
+    # Sec. "Numerical Verification": n = 3, dk = dv = 4, scores divided by
+    # sqrt(4).  The head is zero-padded to d = 64 (zero columns add nothing to
+    # the inner products and give zero output columns), the scale stays 1/2.
+    import json
+    import os
+    with open(os.path.join(golden_dir, "worked_example_n3_d4.json")) as f:
+        g = json.load(f)
+    d = 64
+
+    def pad(a):
+        out = np.zeros((1, 1, 3, d), dtype=np.float32)
+        out[0, 0, :, :4] = np.asarray(a, dtype=np.float32)
+        return out
+    q, k, v = pad(g["Q"]), pad(g["K"]), pad(g["V"])
+    ref = oracle_full(q, k, v, scale=g["scale"])
+    for dtype, tol_oracle in (("f32", 1e-5), ("bf16", 2e-2)):
+        qq, kk, vv = (a if dtype == "f32" else synth.f32_to_bf16_bits(a) for a in (q, k, v))
+        refd = ref if dtype == "f32" else oracle_full(qq, kk, vv, scale=g["scale"])
+        o = run_gpu(qq, kk, vv, scale=g["scale"], out_dtype="f32")
+        assert np.all(o[..., 4:] == 0.0)
+        err = max_err(o, refd)
+        table = max_err(o[0, 0, :, :4], np.asarray(g["O_table2"]))
+        say(f"worked example {dtype}: |O - oracle| {err:.3e}, |O - Table 2| {table:.3e}")
+        assert err <= tol_oracle
+        if dtype == "f32":
+            assert table <= 2e-4
+
+
+# ------------------------------------------ joint K/V row permutation (non-causal)
+
+@pytest.mark.parametrize("shape", [(1, 2, 1, 3000, 128), (2, 2, 300, 517, 64),
+                                   (1, 4, 1000, 1000, 128)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_joint_kv_row_permutation(shape, dtype):
+    # Without a mask the softmax is a sum over keys: permuting the rows of K and
+    # V together leaves O unchanged (up to the summation order).
+    B, H, Nq, Nk, d = shape
+    q, k, v = gen(B, H, Nq, Nk, d, dtype, seed=_seed("perm", shape, dtype))
+    perm = np.random.default_rng(7).permutation(Nk)
+    kp, vp = np.ascontiguousarray(k[:, :, perm]), np.ascontiguousarray(v[:, :, perm])
+    o = run_gpu(q, k, v, out_dtype="f32")
+    op = run_gpu(q, kp, vp, out_dtype="f32")
+    ref = oracle_full(q, k, v)
+    e1, e2, e12 = max_err(o, ref), max_err(op, ref), max_err(o, op)
+    say(f"permutation {shape} {dtype}: {e1:.3e} {e2:.3e} {e12:.3e}")
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype] and e12 <= TOL[dtype]
