@@ -28,7 +28,8 @@
  *      LSE [B][H][Nq] fp32 (optional, NULL = not written)
  *    Every tensor pointer must be 16-byte aligned.
  *  - The library allocates no device memory, keeps no state between calls,
- *    never synchronises, and is safe to call from several host threads.  Work
+ *    never synchronises, and is safe to call from several host threads (the
+ *    one exception: moa_attn_fwd_noalloc's fixed scratch array, below).  Work
  *    is enqueued on `stream` (at most two kernels for the forward, three for
  *    the projected forward and for the backward); errors raised by kernels
  *    surface at the caller's next synchronisation.
@@ -52,7 +53,9 @@ enum {
                                  non-finite scale, causal with Nq > Nk, unknown dtype */
     MOA_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement (head size) */
     MOA_ERR_WORKSPACE = 3,    /* workspace missing or smaller than moa_attn_workspace_bytes() */
-    MOA_ERR_HIP = 4           /* the HIP runtime reported an error while enqueueing */
+    MOA_ERR_HIP = 4,          /* the HIP runtime reported an error while enqueueing */
+    MOA_ERR_SCRATCH = 5       /* moa_attn_fwd_noalloc: the call needs more scratch than the
+                                 library's fixed array holds (MOA_NOALLOC_SCRATCH_BYTES) */
 };
 
 /* Storage types for Q, K, V (in_dtype) and O (out_dtype). */
@@ -171,6 +174,44 @@ int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, f
                          const int64_t* v_strides, const int64_t* o_strides, float scale,
                          int causal, int in_dtype, int out_dtype, void* workspace,
                          size_t workspace_bytes, int num_splits, void* stream);
+
+/* Bytes of the fixed device scratch array of moa_attn_fwd_noalloc, per GPU. */
+#define MOA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/*
+ * moa_attn_fwd_noalloc -- moa_attn_fwd for callers that cannot allocate device
+ * memory: code being captured into a HIP graph, tight serving loops, and
+ * hosts that forbid allocation.  The arguments, results and status codes are
+ * those of moa_attn_fwd without the workspace: the partial states of calls
+ * that split their keys (decode-shaped calls; bf16 prefill on grids too small
+ * to fill the GPU) go to a fixed scratch array in device memory that the
+ * library itself holds, MOA_NOALLOC_SCRATCH_BYTES bytes on every GPU the
+ * library runs on, from the loading of its code until the process ends.
+ * Neither this call nor anything it enqueues allocates or frees device
+ * memory; its device address is looked up (not allocated) on the first call
+ * on each GPU, with that GPU made current for the lookup.
+ *
+ * Limits and sharing:
+ *  - A call whose key splits need more than MOA_NOALLOC_SCRATCH_BYTES of
+ *    partial states (moa_attn_workspace_bytes(...) with the same arguments)
+ *    returns MOA_ERR_SCRATCH: decode-shaped calls, and prefill calls with
+ *    num_splits > 1.  With num_splits == 0 such a prefill call runs in one
+ *    pass instead, exactly as moa_attn_fwd does with too small a workspace.
+ *    The automatic split choice stays within the array for every problem
+ *    size whose partial states need at most 32 MiB (e.g. decode with up to
+ *    B*H = 8192 heads at any Nk, or any prefill whose split items fill one
+ *    wave of workgroups).
+ *  - Every call on one GPU uses that GPU's one array: calls that overlap in
+ *    time on the same GPU (on different streams, or from several host
+ *    threads) race and may return wrong results.  Calls ordered on one stream
+ *    are safe; the array keeps the last call's partial states, and nothing
+ *    in it needs to start at zero.
+ * Results are bit-identical to those of moa_attn_fwd with a workspace.
+ */
+int moa_attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                         float scale, int causal, int in_dtype, int out_dtype, int num_splits,
+                         void* stream);
 
 /*
  * moa_attn_bwd_workspace_bytes -- device workspace a moa_attn_bwd call with

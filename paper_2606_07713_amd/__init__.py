@@ -24,9 +24,12 @@ __all__ = [
     "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd",
     "moa_attn_fwd_strided", "moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "attn_bwd", "LIB_PATH",
     "lib", "moa_attn_fwd_proj", "moa_attn_proj_workspace_bytes", "attn_fwd_proj",
+    "moa_attn_fwd_noalloc", "MOA_ERR_SCRATCH", "MOA_NOALLOC_SCRATCH_BYTES",
 ]
 
 MOA_OK, MOA_ERR_INVALID_ARG, MOA_ERR_UNSUPPORTED, MOA_ERR_WORKSPACE, MOA_ERR_HIP = 0, 1, 2, 3, 4
+MOA_ERR_SCRATCH = 5
+MOA_NOALLOC_SCRATCH_BYTES = 32 << 20
 MOA_F32, MOA_BF16 = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoa_attn.so")
@@ -54,6 +57,9 @@ lib.moa_attn_fwd.restype = _ci
 lib.moa_attn_fwd_strided.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
                                      _vp, _vp, _vp, _vp, _f32, _ci, _ci, _ci, _vp, _sz, _ci, _vp]
 lib.moa_attn_fwd_strided.restype = _ci
+lib.moa_attn_fwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
+                                     _f32, _ci, _ci, _ci, _ci, _vp]
+lib.moa_attn_fwd_noalloc.restype = _ci
 lib.moa_attn_workspace_bytes.argtypes = [_i64] * 6 + [_ci]
 lib.moa_attn_workspace_bytes.restype = _sz
 lib.moa_attn_num_splits.argtypes = [_i64] * 6 + [_ci]
@@ -123,6 +129,14 @@ def moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_str
     return int(lib.moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, *ptrs,
                                         float(scale), int(causal), in_dtype, out_dtype, workspace,
                                         workspace_bytes, num_splits, stream))
+
+
+def moa_attn_fwd_noalloc(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, scale, causal, in_dtype,
+                         out_dtype, num_splits, stream) -> int:
+    """Raw C call of the forward that allocates nothing (key-split partial states go to the
+    library's fixed per-GPU scratch array); pointers are ints or None; returns the status."""
+    return int(lib.moa_attn_fwd_noalloc(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, float(scale),
+                                        int(causal), in_dtype, out_dtype, num_splits, stream))
 
 
 def moa_attn_bwd_workspace_bytes(B, H, Nq, Nk, dk, dv) -> int:

@@ -169,7 +169,18 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
              int64_t Nq, int64_t Nk, int64_t dk, int64_t dv, const int64_t* q_strides,
              const int64_t* k_strides, const int64_t* v_strides, const int64_t* o_strides,
              float scale, int causal, int in_dtype, int out_dtype, void* workspace,
-             size_t workspace_bytes, int num_splits, void* stream) {
+             size_t workspace_bytes, int num_splits, void* stream, bool use_scratch = false) {
+    // use_scratch: the library's fixed scratch array serves as the workspace
+    // (moa_attn_fwd_noalloc); its device address is looked up only after the
+    // validation below, and nothing is allocated.
+    if (use_scratch) {
+        workspace = nullptr;
+        workspace_bytes = moa::kNoallocScratchBytes;
+    }
+    const int short_ws = use_scratch ? MOA_ERR_SCRATCH : MOA_ERR_WORKSPACE;
+    auto ws_fits = [&](size_t need) {
+        return use_scratch ? need <= workspace_bytes : (workspace && workspace_bytes >= need);
+    };
     // ---- validation: no HIP call happens before all of it has passed
     if (!Q || !K || !V || !O) return MOA_ERR_INVALID_ARG;
     if (!dims_ok(B, H, Nq, Nk, dk, dv)) return MOA_ERR_INVALID_ARG;
@@ -217,20 +228,20 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
     if (decode && bh > 0) {
         splits = pick_splits(bh, Nk, num_splits);
         need = decode_ws_bytes(bh, dk, splits);
-        if (!workspace || workspace_bytes < need) return MOA_ERR_WORKSPACE;
+        if (!ws_fits(need)) return short_ws;
     } else if (!decode && bh > 0 && Nq > 0 && in_dtype == MOA_BF16) {
         // Split-K prefill: explicitly requested splits need the workspace;
         // the automatic choice falls back to one pass without it.
         splits = pick_prefill_splits(bh, Nq, Nk, num_splits);
         if (splits > 1 && !prefill_splits_fit(bh, Nq, splits)) return MOA_ERR_UNSUPPORTED;
         need = splits > 1 ? prefill_ws_bytes(bh, Nq, dk, splits) : 0;
-        if (need && (!workspace || workspace_bytes < need)) {
-            if (num_splits > 1) return MOA_ERR_WORKSPACE;
+        if (need && !ws_fits(need)) {
+            if (num_splits > 1) return short_ws;
             splits = 1;
             need = 0;
         }
     }
-    if (need) {
+    if (need && !use_scratch) {
         const size_t wn = need;
         if (overlaps(workspace, wn, O, on) || overlaps(workspace, wn, Q, qn) ||
             overlaps(workspace, wn, K, kn) || overlaps(workspace, wn, V, vn) ||
@@ -238,6 +249,13 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
             return MOA_ERR_INVALID_ARG;
     }
     if (bh == 0 || Nq == 0) return MOA_OK;
+    if (use_scratch && need) {
+        const hipError_t e = moa::noalloc_scratch(static_cast<hipStream_t>(stream), &workspace);
+        if (e != hipSuccess) {
+            g_last_hip_error = hipGetErrorName(e);
+            return MOA_ERR_HIP;
+        }
+    }
 
     moa::Problem p;
     p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
@@ -291,6 +309,14 @@ int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, f
     return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_strides, v_strides,
                     o_strides, scale, causal, in_dtype, out_dtype, workspace, workspace_bytes,
                     num_splits, stream);
+}
+
+int moa_attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                         float scale, int causal, int in_dtype, int out_dtype, int num_splits,
+                         void* stream) {
+    return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, nullptr, nullptr, nullptr, nullptr,
+                    scale, causal, in_dtype, out_dtype, nullptr, 0, num_splits, stream, true);
 }
 
 size_t moa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,
@@ -433,6 +459,9 @@ const char* moa_attn_status_string(int status) {
         case MOA_ERR_UNSUPPORTED: return "unsupported head size or problem size";
         case MOA_ERR_WORKSPACE: return "workspace missing or too small";
         case MOA_ERR_HIP: return "HIP runtime error while enqueueing";
+        case MOA_ERR_SCRATCH:
+            return "problem needs more scratch than the library's fixed array holds "
+                   "(MOA_NOALLOC_SCRATCH_BYTES); use moa_attn_fwd with a workspace";
         default: return "unknown status";
     }
 }

@@ -91,6 +91,14 @@ struct BwdProblem {
 // Backward: row-dot kernel (D), dQ kernel, dK/dV kernel, in stream order.
 hipError_t launch_bwd(const BwdProblem& p, hipStream_t stream);
 
+// Bytes of the fixed device scratch array of moa_attn_fwd_noalloc (one per
+// GPU, held until the process ends; equal to MOA_NOALLOC_SCRATCH_BYTES).
+constexpr size_t kNoallocScratchBytes = size_t(32) << 20;
+
+// Device address of the scratch array on the GPU that runs `stream`, looked up
+// once per device (with that device current) and cached; allocates nothing.
+hipError_t noalloc_scratch(hipStream_t stream, void** ptr);
+
 // Row-tile size of the bf16 prefill kernel (queries per workgroup).
 constexpr int kPrefillBf16RowsPerBlock = 256;
 // Row-tile size of the fp32 prefill kernel.

@@ -18,5 +18,6 @@ hipError_t launch_split_combine(const Problem&, int, const float*, const float*,
 }
 hipError_t launch_bwd(const BwdProblem&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_proj(const ProjProblem&, hipStream_t) { return hipErrorNoDevice; }
+hipError_t noalloc_scratch(hipStream_t, void**) { return hipErrorNoDevice; }
 
 }  // namespace moa

@@ -21,7 +21,8 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = _declared_functions()
     assert names == ["moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "moa_attn_fwd",
-                     "moa_attn_fwd_proj", "moa_attn_fwd_strided", "moa_attn_last_hip_error",
+                     "moa_attn_fwd_noalloc", "moa_attn_fwd_proj", "moa_attn_fwd_strided",
+                     "moa_attn_last_hip_error",
                      "moa_attn_num_splits", "moa_attn_proj_workspace_bytes",
                      "moa_attn_status_string", "moa_attn_workspace_bytes"]
 
@@ -48,7 +49,7 @@ def test_header_is_plain_c():
 
 def test_status_strings():
     assert moa.moa_attn_status_string(moa.MOA_OK) == "ok"
-    for s in (1, 2, 3, 4):
+    for s in (1, 2, 3, 4, 5):
         assert moa.moa_attn_status_string(s) not in ("ok", "unknown status")
     assert moa.moa_attn_status_string(99) == "unknown status"
     assert moa.moa_attn_last_hip_error() == "hipSuccess"
@@ -272,3 +273,36 @@ def test_proj_validation_rejects_before_any_gpu_work(kw, status):
 def test_proj_empty_problems_are_no_ops():
     assert _call_proj(B=0) == moa.MOA_OK
     assert _call_proj(N=0, X=None, O=None, workspace=None) == moa.MOA_OK
+
+
+def _call_noalloc(**kw):
+    # Fake, far-apart, 16-byte-aligned device addresses: every call here is rejected (or
+    # is empty) before anything touches them.
+    base = 1 << 40
+    args = dict(Q=base, K=2 * base, V=3 * base, O=4 * base, LSE=None, B=64, H=32, Nq=1,
+                Nk=8192, dk=128, dv=128, scale=0.125, causal=0, in_dtype=moa.MOA_BF16,
+                out_dtype=moa.MOA_BF16, num_splits=0, stream=None)
+    args.update(kw)
+    return moa.moa_attn_fwd_noalloc(**args)
+
+
+def test_noalloc_validation():
+    assert moa.MOA_NOALLOC_SCRATCH_BYTES == 32 << 20
+    hdr = open(HEADER).read()
+    assert "#define MOA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in hdr
+    # empty problems are valid no-ops; invalid arguments are rejected as by moa_attn_fwd
+    assert _call_noalloc(B=0) == moa.MOA_OK
+    assert _call_noalloc(Nq=0) == moa.MOA_OK
+    assert _call_noalloc(Q=None) == moa.MOA_ERR_INVALID_ARG
+    assert _call_noalloc(Q=(1 << 40) + 8) == moa.MOA_ERR_INVALID_ARG
+    assert _call_noalloc(dk=96, dv=96) == moa.MOA_ERR_UNSUPPORTED
+    assert _call_noalloc(causal=1, Nq=9000, Nk=8192) == moa.MOA_ERR_INVALID_ARG
+    # decode whose partial states exceed the fixed array: 65536 heads x 1 split x 130 floats
+    need = moa.moa_attn_workspace_bytes(256, 256, 1, 256, 128, 128, 0)
+    assert need > moa.MOA_NOALLOC_SCRATCH_BYTES
+    assert _call_noalloc(B=256, H=256, Nk=256) == moa.MOA_ERR_SCRATCH
+    # explicit prefill splits beyond the array are rejected too
+    need = moa.moa_attn_workspace_bytes(1, 32, 2048, 65536, 128, 128, 8)
+    assert need > moa.MOA_NOALLOC_SCRATCH_BYTES
+    assert _call_noalloc(H=32, B=1, Nq=2048, Nk=65536, num_splits=8) == moa.MOA_ERR_SCRATCH
+    assert "MOA_NOALLOC_SCRATCH_BYTES" in moa.moa_attn_status_string(moa.MOA_ERR_SCRATCH)
