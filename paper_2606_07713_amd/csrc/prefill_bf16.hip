@@ -105,7 +105,12 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int grp = wave >> 2;                       // ping-pong: phase group; key split: key half
+    // Key split: the key half decides the buffer descriptors of the tile
+    // loads, so it is made visibly wave-uniform (scalar registers; a per-lane
+    // value there makes the compiler loop over the lanes around every load).
+    // The ping-pong layout keeps its phase group per lane: its register
+    // budget is tighter, and scalar copies of the group cost it spills.
+    const int grp = KSPLIT ? __builtin_amdgcn_readfirstlane(wave >> 2) : wave >> 2;
     const int qw = KSPLIT ? (wave & 3) : wave;       // query block of this wave
     const int lw = KSPLIT ? (wave & 3) : wave;       // index among the waves loading its stream
     const uint32_t g_off = KSPLIT ? (uint32_t)grp * C::TILE_BYTES : 0u;   // stream's slot in a stage
@@ -142,12 +147,22 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         const uint32_t qrb = (uint32_t)A.qr() * 2u;
         const auto rq = make_rsrc(Qh, rows_extent(Nq, qrb, RB));
 #pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+            qf[s] = __builtin_bit_cast(bf16x8, buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16));
+    }
+    // A negative scale flips Q's sign bits once the fragments have arrived;
+    // that happens after the first key tile's load has been issued, so the
+    // two loads are in flight together (no flip: nothing waits for Q before
+    // the first product).
+    auto flip_q = [&]() {
+        if (qflip == 0u) return;
+#pragma unroll
         for (int s = 0; s < D / 16; ++s) {
-            uint4 w = buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16);
-            w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
+            u32x4 w = __builtin_bit_cast(u32x4, qf[s]);
+            w ^= qflip;
             qf[s] = __builtin_bit_cast(bf16x8, w);
         }
-    }
+    };
 
     // Key tiles of this workgroup, of this wave's stream, and of this wave.
     int kv_end = Nk;
@@ -379,6 +394,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // the loads in flight at mid-slot).
     const bool lead = KSPLIT || grp == 0;
     if (g_count > 0) issue_tile_load(true, 0, k_st0);
+    flip_q();
     wait_loads_to_lds();
     __syncthreads();
     for (int t = 0; t <= n_iter; t += 2) {

@@ -141,12 +141,22 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
             const uint32_t qrb = (uint32_t)A.qr() * 2u;
             const auto rq = make_rsrc(Qh, rows_extent(Nq, qrb, RB));
 #pragma unroll
+            for (int s = 0; s < D / 16; ++s)
+                qf[s] = __builtin_bit_cast(bf16x8,
+                                           buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16));
+        }
+        // A negative scale flips Q's sign bits once the fragments have
+        // arrived, after the first stage loads are issued (no flip: nothing
+        // waits for Q before the first product).
+        auto flip_q = [&]() __attribute__((always_inline)) {
+            if (qflip == 0u) return;
+#pragma unroll
             for (int s = 0; s < D / 16; ++s) {
-                uint4 w = buffer_load16(rq, (uint32_t)qrow * qrb + s * 32 + half * 16);
-                w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
+                u32x4 w = __builtin_bit_cast(u32x4, qf[s]);
+                w ^= qflip;
                 qf[s] = __builtin_bit_cast(bf16x8, w);
             }
-        }
+        };
 
         // Steps of the item (over all its waves) and of this wave.
         const int kv_end = CAUSAL ? min(Nk, q0 + BMQ + off) : Nk;
@@ -422,6 +432,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_pipe_kernel(
             load_stage(true, 0, stK);
             load_stage(false, 0, stV);
             load_stage(true, 1, k1);
+            flip_q();
             store_stage(k_r0, stK);
             store_stage(v_r0, stV);
             store_stage(k_r1, k1);

@@ -36,6 +36,8 @@ PREFILL_SHAPES = [
     (2, 1, 200, 1000, 128),    # Nq < Nk: causal is bottom-right aligned
     (1, 1, 1000, 1000, 64),
     (1, 2, 300, 300, 128),
+    (1, 2, 17, 64, 64),        # one full key tile: the single-tile ping-pong launch
+    (1, 2, 64, 64, 128),
 ]
 
 
@@ -165,6 +167,22 @@ def test_unusual_scales(scale, dtype, nq):
     o = run_gpu(q, k, v, causal=True, scale=scale, out_dtype="f32")
     ref = oracle_full(q, k, v, causal=True, scale=scale)
     assert max_err(o, ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 300, 300, 64), (1, 128, 600, 700, 128),
+                                   (4, 64, 1000, 1000, 64)], ids=["keysplit", "pipelined", "pingpong"])
+@pytest.mark.parametrize("causal", [False, True], ids=["full", "causal"])
+def test_negative_scale_layouts(shape, causal):
+    # A negative scale flips the sign of Q inside the kernels (after Q is
+    # loaded); every bf16 prefill layout, sampled rows of the larger two.
+    B, H, Nq, Nk, d = shape
+    q, k, v = gen(B, H, Nq, Nk, d, "bf16", seed=_seed("neg", shape, causal))
+    o = run_gpu(q, k, v, causal=causal, scale=-0.3, out_dtype="f32")
+    rows = sample_rows(B, H, Nq, 256, seed=13, tile=256)
+    ref = oracle.attention_rows(q, k, v, rows, scale=-0.3, causal=causal)
+    err = max_err(o.reshape(-1, d)[rows], ref)
+    say(f"negative scale {shape} causal={causal}: max err {err:.3e}")
+    assert err <= TOL["bf16"]
 
 
 # Key-split (4 items), per-wave pipelined (512 items) and ping-pong (1024 items)
