@@ -153,8 +153,8 @@ int moa_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
  * batch-first layout without a copy), padded rows, packed QKV buffers, and
  * K/V shared across heads (head stride 0).  A stride array may be NULL, which
  * means the contiguous row-major strides of moa_attn_fwd.  LSE stays
- * contiguous [B][H][Nq].  Column-major storage (non-contiguous e) is not
- * supported by this entry point.
+ * contiguous [B][H][Nq].  Column-major storage (non-contiguous e) goes
+ * through moa_attn_fwd_onf instead.
  *
  * Stride rules (elements, each array {batch, head, row}):
  *  - all >= 0 (else MOA_ERR_INVALID_ARG); rows of a tensor with more than one
@@ -174,6 +174,42 @@ int moa_attn_fwd_strided(const void* Q, const void* K, const void* V, void* O, f
                          const int64_t* v_strides, const int64_t* o_strides, float scale,
                          int causal, int in_dtype, int out_dtype, void* workspace,
                          size_t workspace_bytes, int num_splits, void* stream);
+
+/*
+ * moa_attn_fwd_onf -- moa_attn_fwd on tensors with a stride for EVERY
+ * dimension, the head elements included: the storage functions of the
+ * footnote to eq. gamma in full generality, every access at
+ * offset = base + sum_k stride_k * i_k (Def. "Operational Normal Form").
+ * Element (b, h, i, e) of Q lives at
+ *   Q + (b*q_strides[0] + h*q_strides[1] + i*q_strides[2] + e*q_strides[3])
+ * elements, and likewise for K, V and O.  This covers column-major heads
+ * ([B][H][d][N] storage: row stride 1, element stride N), rows that are not
+ * 16-byte aligned, rows that overlap (inputs only), and every layout of
+ * moa_attn_fwd_strided (element stride 1).  A stride array may be NULL: the
+ * contiguous row-major strides.  LSE stays contiguous [B][H][Nq].
+ *
+ * Dispatch: when every tensor has element stride 1 and meets the stride and
+ * alignment rules of moa_attn_fwd_strided, the call is exactly that entry
+ * point's (same kernels, workspace and split rules).  Otherwise an
+ * element-gather kernel serves it: it reads each element at its own address,
+ * computes in fp32 (fp32 or bf16 inputs; fp32 products, exact online
+ * softmax), needs no workspace (workspace, workspace_bytes and num_splits are
+ * then ignored), and runs far below the matrix-core kernels' throughput.
+ *
+ * Rules for the gather path: all strides >= 0 (else MOA_ERR_INVALID_ARG);
+ * Q, K, V aligned to their element size, O to its element size, LSE to 4
+ * bytes; O must not write any element twice (its dimensions of size > 1,
+ * ordered by stride, must nest without overlap); O and LSE must not overlap
+ * any tensor, a tensor occupying the bytes from its base pointer to its last
+ * element.  Q, K and V may overlap one another and themselves.  All other
+ * arguments, results and status codes are those of moa_attn_fwd.
+ */
+int moa_attn_fwd_onf(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                     int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                     const int64_t* q_strides, const int64_t* k_strides, const int64_t* v_strides,
+                     const int64_t* o_strides, float scale, int causal, int in_dtype,
+                     int out_dtype, void* workspace, size_t workspace_bytes, int num_splits,
+                     void* stream);
 
 /* Bytes of the fixed device scratch array of moa_attn_fwd_noalloc, per GPU. */
 #define MOA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)

@@ -24,7 +24,7 @@ __all__ = [
     "moa_attn_num_splits", "moa_attn_status_string", "moa_attn_last_hip_error", "attn_fwd",
     "moa_attn_fwd_strided", "moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "attn_bwd", "LIB_PATH",
     "lib", "moa_attn_fwd_proj", "moa_attn_proj_workspace_bytes", "attn_fwd_proj",
-    "moa_attn_fwd_noalloc", "MOA_ERR_SCRATCH", "MOA_NOALLOC_SCRATCH_BYTES",
+    "moa_attn_fwd_noalloc", "MOA_ERR_SCRATCH", "MOA_NOALLOC_SCRATCH_BYTES", "moa_attn_fwd_onf",
 ]
 
 MOA_OK, MOA_ERR_INVALID_ARG, MOA_ERR_UNSUPPORTED, MOA_ERR_WORKSPACE, MOA_ERR_HIP = 0, 1, 2, 3, 4
@@ -57,6 +57,9 @@ lib.moa_attn_fwd.restype = _ci
 lib.moa_attn_fwd_strided.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
                                      _vp, _vp, _vp, _vp, _f32, _ci, _ci, _ci, _vp, _sz, _ci, _vp]
 lib.moa_attn_fwd_strided.restype = _ci
+lib.moa_attn_fwd_onf.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
+                                 _vp, _vp, _vp, _vp, _f32, _ci, _ci, _ci, _vp, _sz, _ci, _vp]
+lib.moa_attn_fwd_onf.restype = _ci
 lib.moa_attn_fwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
                                      _f32, _ci, _ci, _ci, _ci, _vp]
 lib.moa_attn_fwd_noalloc.restype = _ci
@@ -131,6 +134,27 @@ def moa_attn_fwd_strided(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_str
                                         workspace_bytes, num_splits, stream))
 
 
+def _stride_array4(strides):
+    if strides is None:
+        return None
+    if len(strides) != 4:
+        raise ValueError("a stride array of moa_attn_fwd_onf has four entries: batch, head, row, "
+                         "element")
+    return (ctypes.c_int64 * 4)(*[int(x) for x in strides])
+
+
+def moa_attn_fwd_onf(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q_strides, k_strides, v_strides,
+                     o_strides, scale, causal, in_dtype, out_dtype, workspace, workspace_bytes,
+                     num_splits, stream) -> int:
+    """Raw C call with per-tensor (batch, head, row, element) strides (4-sequences, or None
+    for the contiguous default); returns the status."""
+    arrs = [_stride_array4(x) for x in (q_strides, k_strides, v_strides, o_strides)]
+    ptrs = [ctypes.cast(a, ctypes.c_void_p) if a is not None else None for a in arrs]
+    return int(lib.moa_attn_fwd_onf(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, *ptrs, float(scale),
+                                    int(causal), in_dtype, out_dtype, workspace, workspace_bytes,
+                                    num_splits, stream))
+
+
 def moa_attn_fwd_noalloc(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, scale, causal, in_dtype,
                          out_dtype, num_splits, stream) -> int:
     """Raw C call of the forward that allocates nothing (key-split partial states go to the
@@ -165,10 +189,10 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
              num_splits=0, out=None, workspace=None, stream=None):
     """Fused attention on torch device tensors shaped [B, H, N, d] (same dtype).
 
-    The tensors may be any strided views whose last dimension is contiguous (e.g. a
-    [B, N, H, d] tensor viewed with ``.transpose(1, 2)``, or slices of a packed QKV
-    buffer); their strides go to ``moa_attn_fwd_strided`` and nothing is copied.  ``out``
-    may be such a view too.  Returns O [B, H, Nq, dv] (and LSE [B, H, Nq] fp32 when
+    The tensors may be any strided views (e.g. a [B, N, H, d] tensor viewed with
+    ``.transpose(1, 2)``, slices of a packed QKV buffer, or column-major heads viewed with
+    ``.transpose(2, 3)``); their strides go to ``moa_attn_fwd_onf`` and nothing is copied.  ``out`` may be
+    such a view too.  Returns O [B, H, Nq, dv] (and LSE [B, H, Nq] fp32 when
     ``return_lse``).  ``scale`` defaults to 1/sqrt(dk).  Raises ``MoaAttnError`` on a
     rejected call.
     """
@@ -178,8 +202,6 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
     for t in (q, k, v):
         if not t.is_cuda:
             raise ValueError("q, k, v must be device tensors")
-        if t.stride(3) != 1 and t.shape[3] > 1:
-            raise ValueError("the last dimension of q, k, v must be contiguous")
     if not (q.dtype == k.dtype == v.dtype):
         raise TypeError("q, k, v must share one dtype")
     B, H, Nq, dk = q.shape
@@ -193,10 +215,8 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
         scale = 1.0 / math.sqrt(dk)
     if out is None:
         out = torch.empty((B, H, Nq, dv), dtype=odt, device=q.device)
-    elif (tuple(out.shape) != (B, H, Nq, dv) or out.dtype != odt or out.device != q.device
-          or (out.stride(3) != 1 and dv > 1)):
-        raise ValueError("out must be a [B, H, Nq, dv] tensor of the output dtype whose last "
-                         "dimension is contiguous")
+    elif tuple(out.shape) != (B, H, Nq, dv) or out.dtype != odt or out.device != q.device:
+        raise ValueError("out must be a [B, H, Nq, dv] tensor of the output dtype")
     lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device) if return_lse else None
     ws_bytes = moa_attn_workspace_bytes(B, H, Nq, Nk, dk, dv, num_splits)
     if in_code == MOA_F32 and Nq != 1:
@@ -205,14 +225,14 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    st = moa_attn_fwd_strided(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                              lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv,
-                              q.stride()[:3], k.stride()[:3], v.stride()[:3], out.stride()[:3],
-                              scale, causal, in_code, out_code,
-                              workspace.data_ptr() if workspace is not None else None,
-                              workspace.numel() * workspace.element_size()
-                              if workspace is not None else 0,
-                              num_splits, stream.cuda_stream)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_n = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    # moa_attn_fwd_onf runs layouts the matrix-core kernels read exactly as
+    # moa_attn_fwd_strided does, and the others through its gather kernel.
+    st = moa_attn_fwd_onf(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                          lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv,
+                          q.stride(), k.stride(), v.stride(), out.stride(), scale, causal,
+                          in_code, out_code, ws_ptr, ws_n, num_splits, stream.cuda_stream)
     if st != MOA_OK:
         raise MoaAttnError(st)
     return (out, lse) if return_lse else out

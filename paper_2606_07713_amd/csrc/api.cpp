@@ -135,6 +135,37 @@ bool injective(const Strides& s, int64_t B, int64_t H, int64_t N, int64_t d) {
     return true;
 }
 
+// Element strides of one tensor over (batch, head, row, head element), for
+// moa_attn_fwd_onf.
+struct Strides4 {
+    int64_t s[4];
+};
+
+Strides4 contiguous4(int64_t H, int64_t N, int64_t d) { return {{H * N * d, N * d, d, 1}}; }
+
+// Bytes from a tensor's base pointer to the end of its last element.
+size_t extent4(const Strides4& t, int64_t B, int64_t H, int64_t N, int64_t d, size_t es) {
+    if (B == 0 || H == 0 || N == 0 || d == 0) return 0;
+    return (size_t)((B - 1) * t.s[0] + (H - 1) * t.s[1] + (N - 1) * t.s[2] + (d - 1) * t.s[3] + 1) * es;
+}
+
+// True if no two (batch, head, row, element) positions share an address: the
+// dimensions of size > 1, by increasing stride, nest without overlap.
+bool injective4(const Strides4& t, int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (B == 0 || H == 0 || N == 0 || d == 0) return true;
+    struct Dim { int64_t stride, count; } dims[4] = {{t.s[0], B}, {t.s[1], H}, {t.s[2], N}, {t.s[3], d}};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 4; ++j)
+            if (dims[j].stride < dims[i].stride) { Dim x = dims[i]; dims[i] = dims[j]; dims[j] = x; }
+    int64_t span = 1;   // elements covered by the inner dimensions so far
+    for (int i = 0; i < 4; ++i) {
+        if (dims[i].count <= 1) continue;
+        if (dims[i].stride < span) return false;
+        span = dims[i].stride * dims[i].count;
+    }
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -317,6 +348,89 @@ int moa_attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O, f
                          void* stream) {
     return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, nullptr, nullptr, nullptr, nullptr,
                     scale, causal, in_dtype, out_dtype, nullptr, 0, num_splits, stream, true);
+}
+
+int moa_attn_fwd_onf(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                     int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk, int64_t dv,
+                     const int64_t* q_strides, const int64_t* k_strides, const int64_t* v_strides,
+                     const int64_t* o_strides, float scale, int causal, int in_dtype,
+                     int out_dtype, void* workspace, size_t workspace_bytes, int num_splits,
+                     void* stream) {
+    // ---- validation: no HIP call happens before all of it has passed
+    if (!Q || !K || !V || !O) return MOA_ERR_INVALID_ARG;
+    if (!dims_ok(B, H, Nq, Nk, dk, dv)) return MOA_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return MOA_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1) return MOA_ERR_INVALID_ARG;
+    if (causal && Nq > Nk) return MOA_ERR_INVALID_ARG;
+    if (in_dtype != MOA_F32 && in_dtype != MOA_BF16) return MOA_ERR_INVALID_ARG;
+    if (out_dtype != MOA_F32 && out_dtype != in_dtype) return MOA_ERR_INVALID_ARG;
+    if (num_splits < 0 || num_splits > kMaxSplits) return MOA_ERR_INVALID_ARG;
+    if (!head_supported(dk, dv)) return MOA_ERR_UNSUPPORTED;
+    if (!sizes_fit(B, H, Nq, Nk, dk)) return MOA_ERR_UNSUPPORTED;
+    const Strides4 sq = q_strides ? Strides4{{q_strides[0], q_strides[1], q_strides[2], q_strides[3]}}
+                                  : contiguous4(H, Nq, dk);
+    const Strides4 sk = k_strides ? Strides4{{k_strides[0], k_strides[1], k_strides[2], k_strides[3]}}
+                                  : contiguous4(H, Nk, dk);
+    const Strides4 sv = v_strides ? Strides4{{v_strides[0], v_strides[1], v_strides[2], v_strides[3]}}
+                                  : contiguous4(H, Nk, dv);
+    const Strides4 so = o_strides ? Strides4{{o_strides[0], o_strides[1], o_strides[2], o_strides[3]}}
+                                  : contiguous4(H, Nq, dv);
+    for (const Strides4* t : {&sq, &sk, &sv, &so})
+        for (int i = 0; i < 4; ++i)
+            if (t->s[i] < 0) return MOA_ERR_INVALID_ARG;
+
+    // Layouts the matrix-core kernels read (contiguous head elements, 16-byte
+    // aligned rows, rows of d elements that do not overlap, 32-bit in-head
+    // offsets) go through moa_attn_fwd_strided's path unchanged.
+    const size_t ies = in_dtype == MOA_F32 ? 4 : 2;
+    const size_t oes = out_dtype == MOA_F32 ? 4 : 2;
+    auto fast_ok = [&](const Strides4& t, int64_t N, int64_t d, size_t es) {
+        return t.s[3] == 1 && check_strides(Strides{t.s[0], t.s[1], t.s[2]}, N, d, es) == 0;
+    };
+    if (fast_ok(sq, Nq, dk, ies) && fast_ok(sk, Nk, dk, ies) && fast_ok(sv, Nk, dv, ies) &&
+        fast_ok(so, Nq, dv, oes) && aligned16(Q) && aligned16(K) && aligned16(V) && aligned16(O)) {
+        const int64_t q3[3] = {sq.s[0], sq.s[1], sq.s[2]}, k3[3] = {sk.s[0], sk.s[1], sk.s[2]};
+        const int64_t v3[3] = {sv.s[0], sv.s[1], sv.s[2]}, o3[3] = {so.s[0], so.s[1], so.s[2]};
+        return fwd_impl(Q, K, V, O, LSE, B, H, Nq, Nk, dk, dv, q3, k3, v3, o3, scale, causal,
+                        in_dtype, out_dtype, workspace, workspace_bytes, num_splits, stream);
+    }
+
+    // Element-gather path: any strides; O must not write an element twice.
+    auto aligned_to = [](const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; };
+    if (!aligned_to(Q, ies) || !aligned_to(K, ies) || !aligned_to(V, ies) || !aligned_to(O, oes) ||
+        (LSE && !aligned_to(LSE, 4)))
+        return MOA_ERR_INVALID_ARG;
+    if (!injective4(so, B, H, Nq, dv)) return MOA_ERR_INVALID_ARG;
+    const int64_t bh = B * H;
+    const size_t qn = extent4(sq, B, H, Nq, dk, ies), kn = extent4(sk, B, H, Nk, dk, ies);
+    const size_t vn = extent4(sv, B, H, Nk, dv, ies), on = extent4(so, B, H, Nq, dv, oes);
+    const size_t ln = LSE ? (size_t)bh * Nq * sizeof(float) : 0;
+    if (overlaps(O, on, Q, qn) || overlaps(O, on, K, kn) || overlaps(O, on, V, vn))
+        return MOA_ERR_INVALID_ARG;
+    if (LSE && (overlaps(LSE, ln, O, on) || overlaps(LSE, ln, Q, qn) ||
+                overlaps(LSE, ln, K, kn) || overlaps(LSE, ln, V, vn)))
+        return MOA_ERR_INVALID_ARG;
+    if (bh == 0 || Nq == 0) return MOA_OK;
+
+    moa::Problem p{};
+    p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
+    p.bh = (int)bh; p.nq = (int)Nq; p.nk = (int)Nk; p.d = (int)dk;
+    p.scale = scale;
+    p.causal = causal != 0;
+    p.in_bf16 = in_dtype == MOA_BF16;
+    p.out_bf16 = out_dtype == MOA_BF16;
+    p.splits = 1;
+    moa::GatherLayout g;
+    for (int i = 0; i < 4; ++i) {
+        g.q[i] = sq.s[i]; g.k[i] = sk.s[i]; g.v[i] = sv.s[i]; g.o[i] = so.s[i];
+    }
+    g.H = (int)H;
+    const hipError_t e = moa::launch_prefill_gather(p, g, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = hipGetErrorName(e);
+        return MOA_ERR_HIP;
+    }
+    return MOA_OK;
 }
 
 size_t moa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk,

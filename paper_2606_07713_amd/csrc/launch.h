@@ -47,6 +47,19 @@ inline bool is_contiguous(const Problem& p) {
            L.orow == d && L.oh == nq * d && L.ob == H * nq * d;
 }
 
+// Element strides of Q, K, V and O over (batch, head, row, head element),
+// any non-negative values (a column-major head has row stride 1 and element
+// stride N); the tensors of the gather kernel.
+struct GatherLayout {
+    long long q[4], k[4], v[4], o[4];
+    int H;             // heads, to split a (batch*head) index
+};
+
+// Any layout, fp32 or bf16 inputs, Nq >= 1: one launch of the element-gather
+// kernel (vector ALU, fp32 arithmetic).  Uses p.q/k/v/o/lse, p.bh, p.nq,
+// p.nk, p.d, p.scale, p.causal, p.in_bf16 and p.out_bf16.
+hipError_t launch_prefill_gather(const Problem& p, const GatherLayout& g, hipStream_t stream);
+
 // Prefill, bf16 inputs: one launch of the MFMA tile kernel.
 hipError_t launch_prefill_bf16(const Problem& p, hipStream_t stream);
 
@@ -103,5 +116,7 @@ hipError_t noalloc_scratch(hipStream_t stream, void** ptr);
 constexpr int kPrefillBf16RowsPerBlock = 256;
 // Row-tile size of the fp32 prefill kernel.
 constexpr int kPrefillF32RowsPerBlock = 64;
+// Row-tile size of the element-gather kernel.
+constexpr int kPrefillGatherRowsPerBlock = 64;
 
 }  // namespace moa

@@ -19,5 +19,8 @@ hipError_t launch_split_combine(const Problem&, int, const float*, const float*,
 hipError_t launch_bwd(const BwdProblem&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_proj(const ProjProblem&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t noalloc_scratch(hipStream_t, void**) { return hipErrorNoDevice; }
+hipError_t launch_prefill_gather(const Problem&, const GatherLayout&, hipStream_t) {
+    return hipErrorNoDevice;
+}
 
 }  // namespace moa

@@ -21,7 +21,8 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = _declared_functions()
     assert names == ["moa_attn_bwd", "moa_attn_bwd_workspace_bytes", "moa_attn_fwd",
-                     "moa_attn_fwd_noalloc", "moa_attn_fwd_proj", "moa_attn_fwd_strided",
+                     "moa_attn_fwd_noalloc", "moa_attn_fwd_onf", "moa_attn_fwd_proj",
+                     "moa_attn_fwd_strided",
                      "moa_attn_last_hip_error",
                      "moa_attn_num_splits", "moa_attn_proj_workspace_bytes",
                      "moa_attn_status_string", "moa_attn_workspace_bytes"]
@@ -306,3 +307,45 @@ def test_noalloc_validation():
     assert need > moa.MOA_NOALLOC_SCRATCH_BYTES
     assert _call_noalloc(H=32, B=1, Nq=2048, Nk=65536, num_splits=8) == moa.MOA_ERR_SCRATCH
     assert "MOA_NOALLOC_SCRATCH_BYTES" in moa.moa_attn_status_string(moa.MOA_ERR_SCRATCH)
+
+
+def _call_onf(**kw):
+    # Fake, far-apart device addresses: every call here is rejected (or empty) before
+    # anything touches them.
+    base = 1 << 40
+    args = dict(Q=base, K=2 * base, V=3 * base, O=4 * base, LSE=None, B=2, H=4, Nq=100, Nk=300,
+                dk=64, dv=64, q_strides=None, k_strides=None, v_strides=None, o_strides=None,
+                scale=0.125, causal=0, in_dtype=moa.MOA_BF16, out_dtype=moa.MOA_BF16,
+                workspace=None, workspace_bytes=0, num_splits=0, stream=None)
+    args.update(kw)
+    return moa.moa_attn_fwd_onf(**args)
+
+
+def test_onf_validation():
+    colmajor = lambda H, N, d: (H * d * N, d * N, 1, N)       # [B][H][d][N] storage
+    # empty problems are valid no-ops on either path
+    assert _call_onf(B=0) == moa.MOA_OK
+    assert _call_onf(B=0, k_strides=colmajor(4, 300, 64)) == moa.MOA_OK
+    assert _call_onf(Nq=0, q_strides=colmajor(4, 0, 64)) == moa.MOA_OK
+    # the usual argument checks come first
+    assert _call_onf(Q=None) == moa.MOA_ERR_INVALID_ARG
+    assert _call_onf(dk=96, dv=96) == moa.MOA_ERR_UNSUPPORTED
+    assert _call_onf(causal=1, Nq=400) == moa.MOA_ERR_INVALID_ARG
+    assert _call_onf(in_dtype=7) == moa.MOA_ERR_INVALID_ARG
+    # negative strides are invalid on every dimension
+    for i in range(4):
+        st = list(colmajor(4, 300, 64))
+        st[i] = -1
+        assert _call_onf(B=0 if i == 0 else 2, k_strides=tuple(st)) == moa.MOA_ERR_INVALID_ARG
+    # gather path: element alignment of each pointer
+    assert _call_onf(K=(2 << 40) + 1, k_strides=colmajor(4, 300, 64)) == moa.MOA_ERR_INVALID_ARG
+    assert _call_onf(O=(4 << 40) + 2, out_dtype=moa.MOA_F32,
+                     k_strides=colmajor(4, 300, 64)) == moa.MOA_ERR_INVALID_ARG
+    # gather path: O must not write an element twice (element stride 0, overlapping rows)
+    assert _call_onf(o_strides=(4 * 100 * 64, 100 * 64, 64, 0)) == moa.MOA_ERR_INVALID_ARG
+    assert _call_onf(o_strides=(4 * 100 * 64, 100 * 64, 1, 1)) == moa.MOA_ERR_INVALID_ARG
+    # gather path: O must not overlap an input (column-major O laid over Q's extent)
+    assert _call_onf(O=(1 << 40) + 64, o_strides=colmajor(4, 100, 64),
+                     k_strides=colmajor(4, 300, 64)) == moa.MOA_ERR_INVALID_ARG
+    # LSE must not overlap O either
+    assert _call_onf(LSE=(4 << 40) + 256, k_strides=colmajor(4, 300, 64)) == moa.MOA_ERR_INVALID_ARG

@@ -3,7 +3,11 @@ seeded inputs stored as [B, N, H, d] views, packed QKV buffers, padded rows and
 K/V shared by every head, against the oracle on the contiguous arrays.  Every
 kernel family is covered: the three bf16 prefill layouts (chosen by the number
 of 256-query work items), fp32 prefill and decode.  The layouts are the
-storage functions of the footnote to eq. gamma with per-dimension strides."""
+storage functions of the footnote to eq. gamma with per-dimension strides.
+
+Layouts with a strided head dimension -- column-major heads ([B][H][d][N]),
+rows that are not 16-byte aligned -- go through moa_attn_fwd_onf's
+element-gather kernel; they are checked the same way."""
 import zlib
 
 import numpy as np
@@ -46,6 +50,22 @@ def _views(q, k, v, layout):
         # k, v were generated with one head; every head reads it (head stride 0).
         H = tq.shape[1]
         return tq, tk.expand(-1, H, -1, -1), tv.expand(-1, H, -1, -1)
+    if layout == "colmajor":
+        # every head stored [d][N]: row stride 1, element stride N
+        return tuple(t.transpose(2, 3).contiguous().transpose(2, 3) for t in (tq, tk, tv))
+    if layout == "colmajor_k":
+        return tq, tk.transpose(2, 3).contiguous().transpose(2, 3), tv
+    if layout == "unaligned":
+        # rows of d elements one element apart from the next row's start + 1: not 16-byte aligned
+        out = []
+        for t in (tq, tk, tv):
+            B, H, N, d = t.shape
+            buf = torch.full((B, H, N * (d + 1) + 1), float("nan"), dtype=t.dtype, device=t.device)
+            view = buf[..., 1:].as_strided((B, H, N, d), (H * (N * (d + 1) + 1), N * (d + 1) + 1, d + 1, 1),
+                                           buf.storage_offset() + 1)
+            view.copy_(t)
+            out.append(view)
+        return tuple(out)
     raise ValueError(layout)
 
 
@@ -59,6 +79,8 @@ def _run(q, k, v, layout, out_layout="contiguous", causal=False, out_dtype=None,
     B, H, Nq, dv = tq.shape[0], tq.shape[1], tq.shape[2], tv.shape[3]
     if out_layout == "bshd":
         out = torch.full((B, Nq, H, dv), float("nan"), dtype=odt, device=tq.device).transpose(1, 2)
+    elif out_layout == "colmajor":
+        out = torch.full((B, H, dv, Nq), float("nan"), dtype=odt, device=tq.device).transpose(2, 3)
     else:
         out = None
     r = moa.attn_fwd(tq, tk, tv, causal=causal, out_dtype=odt, out=out, return_lse=return_lse)
@@ -126,6 +148,43 @@ def test_strided_output_bshd(family):
     err = max_err(o.reshape(-1, d)[rows], ref)
     say(f"output bshd {family}: max err {err:.3e}")
     assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("family", list(SHAPES))
+@pytest.mark.parametrize("layout", ["colmajor", "colmajor_k", "unaligned"])
+def test_gathered_inputs_match_oracle(family, layout):
+    """Strided head dimensions and unaligned rows (moa_attn_fwd_onf's gather kernel)."""
+    B, H, Nq, Nk, d, dtype = SHAPES[family]
+    causal = family in ("pipelined", "keysplit", "decode")
+    say(f"gathered layout {layout} family {family} {SHAPES[family]} causal={causal}")
+    q, k, v = gen(B, H, Nq, Nk, d, dtype, _seed("gather", family, layout))
+    for out_dtype in dict.fromkeys((dtype, "f32")):
+        o, lse = _run(q, k, v, layout, causal=causal, out_dtype=out_dtype, return_lse=True)
+        rows = sample_rows(B, H, Nq, 192, seed=17, tile=64)
+        ref, ref_lse = oracle.attention_rows(q, k, v, rows, causal=causal, with_lse=True)
+        err = max_err(o.reshape(-1, d)[rows], ref)
+        lse_err = float(np.abs(lse.reshape(-1)[rows] - ref_lse).max())
+        say(f"  out {out_dtype}: max err {err:.3e}  lse err {lse_err:.3e}")
+        # fp32 arithmetic throughout: fp32 rounding of O (bf16 output: its own rounding)
+        assert err <= (TOL[dtype] if out_dtype == "bf16" else 1e-5)
+        assert lse_err <= 1e-5 * max(1.0, np.abs(ref_lse).max())
+
+
+@pytest.mark.parametrize("family", list(SHAPES))
+def test_gathered_output_colmajor(family):
+    """O written column-major ([B][H][d][N]): every element written (NaN-filled first), from
+    contiguous and from column-major inputs."""
+    B, H, Nq, Nk, d, dtype = SHAPES[family]
+    causal = family != "decode"
+    q, k, v = gen(B, H, Nq, Nk, d, dtype, _seed("out-cm", family))
+    rows = sample_rows(B, H, Nq, 128, seed=18, tile=64)
+    ref = oracle.attention_rows(q, k, v, rows, causal=causal)
+    for layout in ("contiguous", "colmajor"):
+        o = _run(q, k, v, layout, out_layout="colmajor", causal=causal)
+        assert not np.isnan(o).any()
+        err = max_err(o.reshape(-1, d)[rows], ref)
+        say(f"output colmajor {family} from {layout}: max err {err:.3e}")
+        assert err <= TOL[dtype]
 
 
 def test_strided_equals_contiguous_bitwise():
