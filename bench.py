@@ -129,6 +129,36 @@ def _inputs(w, dev):
     return (q, k, v), tuple(synth.to_torch(a, dev) for a in (q, k, v))
 
 
+def library_call(moa, tq, tk, tv, out, w, ws, stream):
+    """One step: a call of the C entry point with its arguments marshalled once beforehand,
+    so that the timed loop measures the library, not the Python wrapper (whose argument
+    checks cost tens of microseconds of host time per call, more than the smaller
+    workloads take on the GPU).  Contiguous tensors go to moa_attn_fwd, strided views to
+    moa_attn_fwd_strided, exactly as attn_fwd would pass them."""
+    import ctypes
+    code = {"torch.float32": moa.MOA_F32, "torch.bfloat16": moa.MOA_BF16}
+    in_code, out_code = code[str(tq.dtype)], code[str(out.dtype)]
+    ptrs = (tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), out.data_ptr(), None)
+    dims = (w.B, w.H, w.Nq, w.Nk, w.dk, w.dv)
+    tail = (ctypes.c_float(w.scale), int(w.causal), in_code, out_code,
+            ws.data_ptr() if ws is not None else None,
+            ws.numel() if ws is not None else 0, 0, stream.cuda_stream)
+    if all(t.is_contiguous() for t in (tq, tk, tv, out)):
+        fn, args = moa.lib.moa_attn_fwd, ptrs + dims + tail
+    else:
+        arrs = [(ctypes.c_int64 * 3)(*t.stride()[:3]) for t in (tq, tk, tv, out)]
+        fn, args = moa.lib.moa_attn_fwd_strided, ptrs + dims + tuple(
+            ctypes.cast(a, ctypes.c_void_p) for a in arrs) + tail
+    keep = (tq, tk, tv, out, ws)
+
+    def call():
+        st = fn(*args)
+        if st != moa.MOA_OK:
+            raise moa.MoaAttnError(st)
+        return keep
+    return call
+
+
 def time_calls(fn, steps: int, warmup: int, stream):
     """Average ms per call over `steps` calls, HIP events on `stream`."""
     import torch
@@ -237,10 +267,9 @@ def main(argv=None):
             out = torch.empty((w.B, w.H, w.Nq, w.dv), dtype=odt, device=dev)
         ws_bytes = moa.moa_attn_workspace_bytes(w.B, w.H, w.Nq, w.Nk, w.dk, w.dv, 0)
         ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
-
-        def call():
-            moa.attn_fwd(tq, tk, tv, scale=w.scale, causal=w.causal, out_dtype=odt, out=out,
-                         workspace=ws if ws_bytes else None, stream=stream)
+        call = library_call(moa, tq, tk, tv, out, w, ws if ws_bytes else None, stream)
+        call()
+        torch.cuda.synchronize()
         ms = time_calls(call, steps or args.steps, args.warmup, stream)
         return w, host, ms, out.element_size()
 

@@ -227,12 +227,21 @@ def attn_fwd(q, k, v, scale=None, causal=False, out_dtype=None, return_lse=False
         stream = torch.cuda.current_stream(q.device)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_n = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    # moa_attn_fwd_onf runs layouts the matrix-core kernels read exactly as
-    # moa_attn_fwd_strided does, and the others through its gather kernel.
-    st = moa_attn_fwd_onf(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                          lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv,
-                          q.stride(), k.stride(), v.stride(), out.stride(), scale, causal,
-                          in_code, out_code, ws_ptr, ws_n, num_splits, stream.cuda_stream)
+    # Contiguous tensors take moa_attn_fwd directly; any other layout goes to
+    # moa_attn_fwd_onf, which runs the layouts the matrix-core kernels read
+    # exactly as moa_attn_fwd_strided does and the others through its gather
+    # kernel.
+    if q.is_contiguous() and k.is_contiguous() and v.is_contiguous() and out.is_contiguous():
+        st = int(lib.moa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                  lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk,
+                                  dv, float(scale), int(causal), in_code, out_code, ws_ptr, ws_n,
+                                  num_splits, stream.cuda_stream))
+    else:
+        st = moa_attn_fwd_onf(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                              lse.data_ptr() if lse is not None else None, B, H, Nq, Nk, dk, dv,
+                              q.stride(), k.stride(), v.stride(), out.stride(), scale,
+                              causal, in_code, out_code, ws_ptr, ws_n, num_splits,
+                              stream.cuda_stream)
     if st != MOA_OK:
         raise MoaAttnError(st)
     return (out, lse) if return_lse else out
