@@ -95,7 +95,8 @@ def test_prefill_pingpong_layout_sampled(shape, causal):
 
 
 PIPE_SHAPES = [
-    # B, H, Nq, Nk, d   (256 <= B*H*ceil(Nq/256) < 1024)
+    # B, H, Nq, Nk, d   (256 <= B*H*ceil(Nq/256) < 1024: the per-wave pipelined kernel, except
+    # causal at d = 128, which takes the ping-pong layout)
     (2, 64, 1000, 1000, 64),
     (1, 128, 600, 700, 128),
     (4, 16, 1024, 1024, 128),
