@@ -115,7 +115,7 @@ hipError_t noalloc_scratch(hipStream_t stream, void** ptr);
 // Row-tile size of the bf16 prefill kernel (queries per workgroup).
 constexpr int kPrefillBf16RowsPerBlock = 256;
 // Row-tile size of the fp32 prefill kernel.
-constexpr int kPrefillF32RowsPerBlock = 64;
+constexpr int kPrefillF32RowsPerBlock = 16;
 // Row-tile size of the element-gather kernel.
 constexpr int kPrefillGatherRowsPerBlock = 64;
 

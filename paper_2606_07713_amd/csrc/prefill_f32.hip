@@ -3,19 +3,24 @@
 //
 // Used where the inputs are fp32 and the result must stay within fp32
 // rounding of the exact attention (no bf16 rounding of any operand).  One
-// workgroup owns 64 queries of one (batch*head); each query row is handled by
-// a quad of 4 lanes that split d, and K/V tiles of 32 keys are staged in LDS
-// and read by all quads as broadcasts.  Scores, the running max and sum and
-// the exponentials stay in registers (DNF eqs. dnf_attn / output_dnf); only O
-// (and optional LSE) are written.
+// workgroup owns 16 queries of one (batch*head); each query row is handled by
+// a quad of 4 lanes that split d.  The four waves of a workgroup hold the same
+// queries and walk disjoint key streams (wave w takes 32-key tiles w, w + 4,
+// ...), each staging its own K/V tiles in its own LDS area, read by its quads
+// as broadcasts; at the end waves 1..3 hand their softmax state to wave 0,
+// which merges it exactly.  The key split keeps the chain of dependent tile
+// loads short, which is what these small problems are bound by.  Scores, the
+// running max and sum and the exponentials stay in registers (DNF eqs.
+// dnf_attn / output_dnf); only O (and optional LSE) are written.
 #include "device_common.h"
 #include "launch.h"
 
 namespace moa {
 namespace {
 
-constexpr int ROWS = 64;          // queries per workgroup
-constexpr int THREADS = ROWS * 4;
+constexpr int ROWS = 16;          // queries per workgroup
+constexpr int STREAMS = 4;        // key streams (waves) per workgroup
+constexpr int THREADS = ROWS * 4 * STREAMS;
 constexpr int KT = 32;            // keys per tile
 
 template <int D, bool CAUSAL>
@@ -24,20 +29,24 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
     float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c,
     Layout L) {
     constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
-    __shared__ __attribute__((aligned(16))) float Ks[KT * D];
-    __shared__ __attribute__((aligned(16))) float Vs[KT * D];
+    // Per wave: its K and V tile; reused at the end for the merge.
+    __shared__ __attribute__((aligned(16))) float Ks[STREAMS][KT * D];
+    __shared__ __attribute__((aligned(16))) float Vs[STREAMS][KT * D];
 
-    const int tid = threadIdx.x;
-    const int quad = tid & 3;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // key stream
+    const int quad = lane & 3;
     const int bh = blockIdx.x / n_qtiles;
     const int qt = blockIdx.x % n_qtiles;
-    const int qrow = qt * ROWS + (tid >> 2);
+    const int qrow = qt * ROWS + (lane >> 2);
     const int qrow_c = qrow < Nq ? qrow : Nq - 1;
     const int off = Nk - Nq;
 
     const float* Qh = Q + head_offset(bh, L.H, L.qb, L.qh);
     const float* Kh = K + head_offset(bh, L.H, L.kb, L.kh);
     const float* Vh = V + head_offset(bh, L.H, L.vb, L.vh);
+    float* ks = Ks[wave];
+    float* vs = Vs[wave];
 
     float4 qv[CH], acc[CH];
 #pragma unroll
@@ -51,18 +60,31 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
     if (CAUSAL) kv_end = min(Nk, qt * ROWS + ROWS + off);
     const int n_kt = (kv_end + KT - 1) / KT;
 
-    for (int kt = 0; kt < n_kt; ++kt) {
+    for (int kt = wave; kt < n_kt; kt += STREAMS) {
         const int kbase = kt * KT;
-        __syncthreads();
-        for (int idx = tid; idx < KT * D / 4; idx += THREADS) {
+        // This wave's tile: its own LDS area, so only its own accesses need
+        // ordering (every lane's previous reads are consumed, its stores land
+        // before the reads below).
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        constexpr int PER = KT * D / 4 / 64;  // float4 per lane per tile
+        float4 kst[PER], vst[PER];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = i * 64 + lane;
             const int row = idx / (D / 4), ch = idx % (D / 4);
             const int key = min(kbase + row, Nk - 1);
-            *reinterpret_cast<float4*>(&Ks[row * D + ch * 4]) =
-                *reinterpret_cast<const float4*>(Kh + (size_t)key * L.kr + ch * 4);
-            *reinterpret_cast<float4*>(&Vs[row * D + ch * 4]) =
-                *reinterpret_cast<const float4*>(Vh + (size_t)key * L.vr + ch * 4);
+            kst[i] = *reinterpret_cast<const float4*>(Kh + (size_t)key * L.kr + ch * 4);
+            vst[i] = *reinterpret_cast<const float4*>(Vh + (size_t)key * L.vr + ch * 4);
         }
-        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = i * 64 + lane;
+            const int row = idx / (D / 4), ch = idx % (D / 4);
+            *reinterpret_cast<float4*>(&ks[row * D + ch * 4]) = kst[i];
+            *reinterpret_cast<float4*>(&vs[row * D + ch * 4]) = vst[i];
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the stores have landed
+        __builtin_amdgcn_wave_barrier();
 
         // scores of this tile, in log2 units (t = c * <q, k>)
         float t[KT];
@@ -72,7 +94,7 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
             float part = 0.0f;
 #pragma unroll
             for (int h = 0; h < CH; ++h) {
-                const float4 kk = *reinterpret_cast<const float4*>(&Ks[j * D + (h * 4 + quad) * 4]);
+                const float4 kk = *reinterpret_cast<const float4*>(&ks[j * D + (h * 4 + quad) * 4]);
                 part = __builtin_fmaf(qv[h].x, kk.x, part);
                 part = __builtin_fmaf(qv[h].y, kk.y, part);
                 part = __builtin_fmaf(qv[h].z, kk.z, part);
@@ -100,13 +122,44 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
             l_run += p;
 #pragma unroll
             for (int h = 0; h < CH; ++h) {
-                const float4 vv = *reinterpret_cast<const float4*>(&Vs[j * D + (h * 4 + quad) * 4]);
+                const float4 vv = *reinterpret_cast<const float4*>(&vs[j * D + (h * 4 + quad) * 4]);
                 acc[h].x = __builtin_fmaf(p, vv.x, acc[h].x);
                 acc[h].y = __builtin_fmaf(p, vv.y, acc[h].y);
                 acc[h].z = __builtin_fmaf(p, vv.z, acc[h].z);
                 acc[h].w = __builtin_fmaf(p, vv.w, acc[h].w);
             }
         }
+    }
+
+    // Waves 1..3 hand (m, l, acc) to wave 0 through their K areas; wave 0
+    // merges exactly: M = max(m0, mw), acc = 2^(m0-M) acc0 + 2^(mw-M) accw,
+    // l likewise.  A stream without visible keys has m = -inf and adds nothing.
+    __syncthreads();
+    if (wave != 0) {
+#pragma unroll
+        for (int h = 0; h < CH; ++h)
+            *reinterpret_cast<float4*>(&ks[(h * 64 + lane) * 4]) = acc[h];
+        vs[lane] = m_run;
+        vs[64 + lane] = l_run;
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w = 1; w < STREAMS; ++w) {
+        const float m1 = Vs[w][lane], l1 = Vs[w][64 + lane];
+        const float mm = fmaxf(m_run, m1);
+        const float a0 = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - mm);
+        const float a1 = (m1 == kNegInf) ? 0.0f : exp2_hw(m1 - mm);
+        l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+        for (int h = 0; h < CH; ++h) {
+            const float4 o = *reinterpret_cast<const float4*>(&Ks[w][(h * 64 + lane) * 4]);
+            acc[h].x = acc[h].x * a0 + o.x * a1;
+            acc[h].y = acc[h].y * a0 + o.y * a1;
+            acc[h].z = acc[h].z * a0 + o.z * a1;
+            acc[h].w = acc[h].w * a0 + o.w * a1;
+        }
+        m_run = mm;
     }
 
     if (qrow < Nq) {
