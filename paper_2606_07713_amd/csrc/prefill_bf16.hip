@@ -234,6 +234,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     f32x16 sacc[BN / 32];            // S^T of the current tile
     bf16x8 pbuf[BN / 16];            // bf16 P^T of the current tile
     float m_run = kNegInf;           // running reference max, log2 units (scores * c)
+    float neg_m = 0.0f;              // -m_run, or 0 while m_run is -inf (no visible key yet)
     float l_run = 0.0f;              // partial denominator over this half-wave's keys
     float alpha_pend = 1.0f;         // rescale owed to oacc before the next P.V
     bool rescale_pend = false;
@@ -279,10 +280,10 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // weights (v_dot2_f32_bf16 against ones), so numerator and denominator use
     // the same p.  exp_pack() returns the tile's partial sum (this lane's 32
     // keys).  Masked scores are -inf and c > 0, so their weight is exactly 0.
-    auto exp_pack = [&](float neg_m) {
+    auto exp_pack = [&](float nm) {
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-        float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        float part[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
@@ -291,15 +292,15 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int i = g * 8 + 2 * j;
-                    const float p0 = exp2_hw(__builtin_fmaf(sacc[kb][i], c, neg_m));
-                    const float p1 = exp2_hw(__builtin_fmaf(sacc[kb][i + 1], c, neg_m));
+                    const float p0 = exp2_hw(__builtin_fmaf(sacc[kb][i], c, nm));
+                    const float p1 = exp2_hw(__builtin_fmaf(sacc[kb][i + 1], c, nm));
                     const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
                     w[j] = __builtin_bit_cast(uint32_t, pp);
-                    part[j] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, part[j], false);
+                    part[j & 1] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, part[j & 1], false);
                 }
                 pbuf[kb * 2 + g] = __builtin_bit_cast(bf16x8, w);
             }
-        return (part[0] + part[1]) + (part[2] + part[3]);
+        return part[0] + part[1];
     };
 
     // Causal / ragged tiles: scores of keys this query must not see become
@@ -339,6 +340,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
             alpha_pend = rescale_pend ? alpha_pend * alpha : alpha;
             rescale_pend = true;
             m_run = m_new;
+            neg_m = (m_new == kNegInf) ? 0.0f : -m_new;
         }
     };
 
@@ -351,22 +353,21 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     // reference without computing the tile max; only if a partial sum exceeds
     // kFastSumLimit (or overflowed) is the reference raised and the tile
     // redone.  Any reference gives the same quotient, so this is exact.  A
-    // row that has seen no key yet starts from its tile max plus
-    // kRefHeadroom instead (a guessed reference far above its scores would
-    // underflow every weight); rows
-    // still without a visible key take reference 0, all their scores being
-    // -inf.  The pass loop
-    // is not unrolled so that pbuf has a single producer.
+    // row that has seen no key yet starts from its tile max plus kRefHeadroom
+    // instead (a guessed reference far above its scores would underflow every
+    // weight); rows still without a visible key keep reference -inf and take
+    // weights 2^(s c) (neg_m = 0), all their scores being -inf.  The redo is a
+    // second straight-line pass; the fast path then carries no copies of the
+    // softmax state (a two-pass loop made the compiler copy m, l and the
+    // rescale factor at every tile).
     auto softmax_phase = [&](int t) {
         if (t >= n_w) return;
         if (tile_needs_mask(t)) apply_mask(t);
         if (wave_any(m_run == kNegInf)) raise_reference();
-        float part;
-#pragma clang loop unroll(disable)
-        for (int pass = 0;; ++pass) {
-            part = exp_pack(m_run == kNegInf ? 0.0f : -m_run);
-            if (pass == 1 || !wave_any(!(part <= kFastSumLimit))) break;
+        float part = exp_pack(neg_m);
+        if (wave_any(!(part <= kFastSumLimit))) {
             raise_reference();
+            part = exp_pack(neg_m);
         }
         l_run += part;
     };
