@@ -69,8 +69,7 @@ def compulsory_bytes(w, out_bytes: int) -> int:
 
 
 KERNEL_SOURCES = {
-    "prefill_bf16": ("prefill_bf16.hip", "prefill_bf16_pipe.hip", "prefill_bf16_common.h",
-                     "device_common.h", "launch.h"),
+    "prefill_bf16": ("prefill_bf16.hip", "prefill_bf16_common.h", "device_common.h", "launch.h"),
     "decode_split": ("decode.hip", "device_common.h", "launch.h"),
 }
 

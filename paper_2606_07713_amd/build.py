@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libmoa_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "prefill_bf16.hip", "prefill_bf16_pipe.hip", "prefill_f32.hip", "decode.hip",
+SOURCES = ["api.cpp", "prefill_bf16.hip", "prefill_f32.hip", "decode.hip",
            "combine.hip", "bwd.hip", "proj.hip", "noalloc.hip", "prefill_gather.hip"]
 
 # Packed fp32 instructions are disabled for all device code on purpose.

@@ -63,8 +63,6 @@ hipError_t launch_prefill_gather(const Problem& p, const GatherLayout& g, hipStr
 // Prefill, bf16 inputs: one launch of the MFMA tile kernel.
 hipError_t launch_prefill_bf16(const Problem& p, hipStream_t stream);
 
-// Prefill, bf16 inputs: one launch of the per-wave pipelined MFMA kernel.
-hipError_t launch_prefill_bf16_pipe(const Problem& p, hipStream_t stream);
 
 // Prefill, fp32 inputs: one launch of the fp32 vector-ALU tile kernel.
 hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream);

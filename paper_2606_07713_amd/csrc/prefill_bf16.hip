@@ -508,14 +508,28 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     }
 }
 
-// Layout choice by the number of 256-query work items.  From
-// kPingPongFromItems on, the ping-pong layout is the fastest measured; from
-// one item per compute unit on, the per-wave pipelined kernel (or, causal at
-// d = 128, the ping-pong layout again: 2-4% faster there, e.g. 153 against
-// 158 us on B2 H16 4K; the pipelined kernel stays 2-10% ahead without the
-// mask and at d = 64); below that the key-split layout, which halves the
-// queries per item to double the items.
-constexpr long long kPingPongFromItems = 1024;
+// Layout choice.  Work items are 256-query tiles (ping-pong) or 128-query
+// tiles (key split: two key streams per workgroup and an exact merge, which
+// doubles the items of a grid).  With the causal mask the snake deal balances
+// unequal items, and the ping-pong layout is the faster one from one item per
+// compute unit on (e.g. B1 H80 1K d = 128: 37.9 against 46.1 us).  Without it
+// every item costs the same, so a grid runs in whole rounds of items per
+// compute unit.  The key split halves the rounds of a grid smaller than the
+// GPU (B4 H8 1K d = 64: 17.2 against 24.9 us), and evens out grids of one to
+// two items per compute unit when its half-size items need at most three
+// quarters of the ping-pong's rounds and every key stream gets at least 512
+// keys (B1 H80 1K: 66.8 against 71.8 us at d = 128, 39.5 against 44.4 at
+// d = 64; with 700 keys the ping-pong layout stays ahead, 56.2 against 58.0
+// us on B1 H128 600 x 700).  Otherwise the ping-pong layout (B1 H48 1K
+// d = 128: 40.7 against 47.9 us; B1 H128 1K: 79.5 against 89.9).
+template <bool CAUSAL>
+bool use_key_split(long long items_pp, long long items_ks, int nk, int cus) {
+    if (items_pp < cus) return true;
+    if (CAUSAL || nk < 1024) return false;
+    const long long rounds_pp2 = 2 * ((items_pp + cus - 1) / cus);   // in key-split item units
+    const long long rounds_ks2 = (items_ks + cus - 1) / cus;
+    return 4 * rounds_ks2 <= 3 * rounds_pp2;
+}
 
 // One persistent launch: as many workgroups as the device holds at once, at
 // most one per work item.  `n_qtiles` counts query tiles times key splits;
@@ -554,20 +568,14 @@ hipError_t launch(const Problem& p, hipStream_t stream) {
         if (e != hipSuccess) return e;
         return launch_split_combine(p, p.splits, ws_acc, ws_ml, stream);
     }
-    const long long items = (long long)p.bh * qt_pp;
-    if (items >= kPingPongFromItems || p.nk <= BN)
-        return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, p.o, p.lse, 1,
-                                                                      stream);
     int cus = 0;
     const hipError_t e = device_cus(stream, cus);
     if (e != hipSuccess) return e;
-    if (items >= cus) {
-        if (CAUSAL && D == 128)
-            return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, p.o, p.lse,
-                                                                          1, stream);
-        return launch_prefill_bf16_pipe(p, stream);
-    }
-    return launch_persistent<D, CAUSAL, OUT_BF16, true, STRIDED>(p, qt_ks, c, p.o, p.lse, 1, stream);
+    if (p.nk > BN &&
+        use_key_split<CAUSAL>((long long)p.bh * qt_pp, (long long)p.bh * qt_ks, p.nk, cus))
+        return launch_persistent<D, CAUSAL, OUT_BF16, true, STRIDED>(p, qt_ks, c, p.o, p.lse, 1,
+                                                                     stream);
+    return launch_persistent<D, CAUSAL, OUT_BF16, false, STRIDED>(p, qt_pp, c, p.o, p.lse, 1, stream);
 }
 
 template <int D, bool STRIDED>

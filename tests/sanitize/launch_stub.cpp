@@ -10,7 +10,6 @@
 namespace moa {
 
 hipError_t launch_prefill_bf16(const Problem&, hipStream_t) { return hipErrorNoDevice; }
-hipError_t launch_prefill_bf16_pipe(const Problem&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_prefill_f32(const Problem&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_decode(const Problem&, int, float*, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_split_combine(const Problem&, int, const float*, const float*, hipStream_t) {
