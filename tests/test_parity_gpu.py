@@ -189,8 +189,8 @@ def test_negative_scale_layouts(shape, causal):
     assert err <= TOL["bf16"]
 
 
-# Key-split (4 items), per-wave pipelined (512 items) and ping-pong (1024 items)
-# layouts; the two larger ones are checked on sampled rows.
+# Key-split (4 items) and ping-pong (512 and 1024 items) layouts; the two
+# larger grids are checked on sampled rows.
 EXTREME_SHAPES = [
     # B, H, Nq, Nk, d
     (2, 2, 77, 700, 128),
