@@ -4,12 +4,14 @@
 // Used where the inputs are fp32 and the result must stay within fp32
 // rounding of the exact attention (no bf16 rounding of any operand).  One
 // workgroup owns 16 queries of one (batch*head); each query row is handled by
-// a quad of 4 lanes that split d.  The four waves of a workgroup hold the same
-// queries and walk disjoint key streams (wave w takes 32-key tiles w, w + 4,
-// ...), each staging its own K/V tiles in its own LDS area, read by its quads
-// as broadcasts; at the end waves 1..3 hand their softmax state to wave 0,
-// which merges it exactly.  The key split keeps the chain of dependent tile
-// loads short, which is what these small problems are bound by.  Scores, the
+// a quad of 4 lanes that split d.  The eight waves of a workgroup hold the
+// same queries and walk disjoint key streams (wave w takes 16-key tiles w,
+// w + 8, ...), each staging its own K/V tiles in its own LDS area, read by its
+// quads as broadcasts; at the end waves 1..7 hand their softmax state to wave
+// 0, which merges it exactly.  The key split keeps each wave's chain of
+// dependent loads and vector instructions short, which is what these small
+// problems are bound by (8 streams of 16 keys measured 24-40% faster than 4
+// streams of 32 keys, on 128 x 128 single heads up to 1K causal grids).  Scores, the
 // running max and sum and the exponentials stay in registers (DNF eqs.
 // dnf_attn / output_dnf); only O (and optional LSE) are written.
 #include "device_common.h"
@@ -19,9 +21,9 @@ namespace moa {
 namespace {
 
 constexpr int ROWS = 16;          // queries per workgroup
-constexpr int STREAMS = 4;        // key streams (waves) per workgroup
+constexpr int STREAMS = 8;        // key streams (waves) per workgroup
 constexpr int THREADS = ROWS * 4 * STREAMS;
-constexpr int KT = 32;            // keys per tile
+constexpr int KT = 16;            // keys per tile
 
 template <int D, bool CAUSAL>
 __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
@@ -29,7 +31,9 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
     float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c,
     Layout L) {
     constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
-    // Per wave: its K and V tile; reused at the end for the merge.
+    // Per wave: its K and V tile; reused at the end for the merge, where a K
+    // tile holds the wave's O (D / 4 floats per lane: KT >= 16 keys).
+    static_assert(KT * D >= 64 * (D / 4), "a K tile must hold one wave's O for the merge");
     __shared__ __attribute__((aligned(16))) float Ks[STREAMS][KT * D];
     __shared__ __attribute__((aligned(16))) float Vs[STREAMS][KT * D];
 
@@ -131,7 +135,7 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
         }
     }
 
-    // Waves 1..3 hand (m, l, acc) to wave 0 through their K areas; wave 0
+    // Waves 1..7 hand (m, l, acc) to wave 0 through their K areas; wave 0
     // merges exactly: M = max(m0, mw), acc = 2^(m0-M) acc0 + 2^(mw-M) accw,
     // l likewise.  A stream without visible keys has m = -inf and adds nothing.
     __syncthreads();
