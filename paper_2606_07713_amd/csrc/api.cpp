@@ -13,9 +13,13 @@ namespace {
 
 constexpr int kMaxSplits = 256;
 // Keys a decode workgroup should stream at least, and the workgroup count the
-// automatic split choice aims for (several waves of workgroups per CU).
+// automatic split choice aims for: one per compute unit of an MI355X (256).
+// Fewer, longer key chunks stream faster than many short ones, e.g. 4 splits
+// of B8 H8 Nk 65536 read 7.1 TB/s against 6.0 with 128, 8 splits of B1 H32
+// Nk 131072 6.6 against 5.1 with 256; grids of 256 or more rows take one
+// split.  (A constant: the workspace size query has no device to ask.)
 constexpr int64_t kMinKeysPerSplit = 256;
-constexpr int64_t kTargetDecodeBlocks = 8192;
+constexpr int64_t kTargetDecodeBlocks = 256;
 // Prefill (Nq > 1, bf16): keys are split across workgroups when fewer than
 // kPrefillSplitBelowItems 256-query items exist (half the 256 compute units
 // of an MI355X), aiming at kPrefillTargetBlocks 128-query split items, each

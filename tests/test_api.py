@@ -82,6 +82,12 @@ def test_workspace_and_splits():
     assert moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 5) >= 64 * 32 * 5 * 130 * 4
     # short key ranges are not split below the minimum chunk
     assert moa.moa_attn_num_splits(1, 1, 1, 100, 64, 64, 0) == 1
+    # decode aims at one workgroup per compute unit (256): B*H*splits >= 256
+    assert moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 0) == 1
+    assert moa.moa_attn_num_splits(4, 32, 1, 32768, 128, 128, 0) == 2
+    assert moa.moa_attn_num_splits(8, 8, 1, 65536, 128, 128, 0) == 4
+    assert moa.moa_attn_num_splits(1, 32, 1, 131072, 128, 128, 0) == 8
+    assert moa.moa_attn_num_splits(1, 1, 1, 1024, 128, 128, 0) == 4       # capped by Nk / 256
     assert moa.moa_attn_workspace_bytes(1, 1, 1, 8192, 96, 96, 0) == 0   # unsupported head
 
 
