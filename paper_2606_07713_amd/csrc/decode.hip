@@ -64,12 +64,16 @@ __device__ __forceinline__ void merge_xor(float& m, float& l, float (&acc)[EPL])
     m = mm;
 }
 
-// a8: one workgroup = one key chunk of one (batch*head).
-template <typename T, int D>
+// a8: one workgroup = one key chunk of one (batch*head).  DIRECT (one chunk
+// per row): the workgroup holds the row's whole softmax state, so it writes
+// O = acc / l (and LSE) itself -- the value the combine pass would compute
+// from a single split, where every merge weight is exactly 1 -- instead of
+// the partial state, and no combine pass runs.
+template <typename T, int D, bool DIRECT = false, bool OUT_BF16 = false>
 __global__ __launch_bounds__(THREADS) void decode_split_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int Nk, int splits,
-    int keys_per_split, float c, Layout L) {
+    int keys_per_split, float c, Layout L, void* __restrict__ Out, float* __restrict__ LSE) {
     using C = Cfg<T, D>;
     constexpr int EPL = C::EPL, LPR = C::LPR, RPW = C::RPW, STEP = C::STEP;
     __shared__ float red_m[WAVES], red_l[WAVES];
@@ -162,12 +166,25 @@ __global__ __launch_bounds__(THREADS) void decode_split_kernel(
 #pragma unroll
             for (int e = 0; e < EPL; ++e) o[e] += a * red_acc[w][el * EPL + e];
         }
-        const size_t row = (size_t)bh * splits + sp;
+        if constexpr (DIRECT) {
+            const float inv = 1.0f / ll;
+            const size_t base = (size_t)head_offset(bh, L.H, L.ob, L.oh) + (size_t)el * EPL;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) ws_acc[row * D + el * EPL + e] = o[e];
-        if (lane == 0) {
-            ws_ml[row * 2 + 0] = mm;
-            ws_ml[row * 2 + 1] = ll;
+            for (int e = 0; e < EPL; ++e) {
+                if constexpr (OUT_BF16)
+                    static_cast<u16*>(Out)[base + e] = (u16)f32_to_bf16_bits(o[e] * inv);
+                else
+                    static_cast<float*>(Out)[base + e] = o[e] * inv;
+            }
+            if (LSE != nullptr && lane == 0) LSE[bh] = (mm + __log2f(ll)) * kLn2;
+        } else {
+            const size_t row = (size_t)bh * splits + sp;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) ws_acc[row * D + el * EPL + e] = o[e];
+            if (lane == 0) {
+                ws_ml[row * 2 + 0] = mm;
+                ws_ml[row * 2 + 1] = ll;
+            }
         }
     }
 }
@@ -178,10 +195,16 @@ hipError_t launch_t(const Problem& p, int splits, float* ws, hipStream_t stream)
     float* ws_acc = ws;
     float* ws_ml = ws + (size_t)p.bh * splits * D;
     const long long blocks = (long long)p.bh * splits;
-    hipError_t e = launch_kernel(decode_split_kernel<T, D>, dim3((unsigned)blocks), dim3(THREADS),
-                                 stream, static_cast<const T*>(p.q), static_cast<const T*>(p.k),
-                                 static_cast<const T*>(p.v), ws_acc, ws_ml, p.nk, splits, kps,
-                                 p.scale * kLog2e, p.lay);
+    const auto args = [&](auto kernel) {
+        return launch_kernel(kernel, dim3((unsigned)blocks), dim3(THREADS), stream,
+                             static_cast<const T*>(p.q), static_cast<const T*>(p.k),
+                             static_cast<const T*>(p.v), ws_acc, ws_ml, p.nk, splits, kps,
+                             p.scale * kLog2e, p.lay, p.o, p.lse);
+    };
+    if (splits == 1)
+        return p.out_bf16 ? args(decode_split_kernel<T, D, true, true>)
+                          : args(decode_split_kernel<T, D, true, false>);
+    const hipError_t e = args(decode_split_kernel<T, D>);
     if (e != hipSuccess) return e;
     // a9: exact merge of the per-chunk states (one query row per batch*head).
     return launch_split_combine(p, splits, ws_acc, ws_ml, stream);
