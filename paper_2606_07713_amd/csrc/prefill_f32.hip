@@ -4,16 +4,16 @@
 // Used where the inputs are fp32 and the result must stay within fp32
 // rounding of the exact attention (no bf16 rounding of any operand).  One
 // workgroup owns 16 queries of one (batch*head); each query row is handled by
-// a quad of 4 lanes that split d.  The eight waves of a workgroup hold the
-// same queries and walk disjoint key streams (wave w takes 16-key tiles w,
-// w + 8, ...), each staging its own K/V tiles in its own LDS area, read by its
-// quads as broadcasts; at the end waves 1..7 hand their softmax state to wave
-// 0, which merges it exactly.  The key split keeps each wave's chain of
-// dependent loads and vector instructions short, which is what these small
-// problems are bound by (8 streams of 16 keys measured 24-40% faster than 4
-// streams of 32 keys, on 128 x 128 single heads up to 1K causal grids).  Scores, the
-// running max and sum and the exponentials stay in registers (DNF eqs.
-// dnf_attn / output_dnf); only O (and optional LSE) are written.
+// a quad of 4 lanes that split d.  The waves of a workgroup (8, or 16 for long
+// keys on small grids) hold the same queries and walk disjoint key streams
+// (wave w takes tiles w, w + STREAMS, ...; 128 keys per round of the
+// workgroup), each staging its own K/V tiles in its own LDS area, read by its
+// quads as broadcasts.  At the end every wave stores its softmax state and all
+// threads merge the streams exactly, one float4 of O each.  The key split
+// keeps each wave's chain of dependent loads and vector instructions short,
+// which is what these small problems are bound by.  Scores, the running max
+// and sum and the exponentials stay in registers (DNF eqs. dnf_attn /
+// output_dnf); only O (and optional LSE) are written.
 #include "device_common.h"
 #include "launch.h"
 
@@ -21,36 +21,43 @@ namespace moa {
 namespace {
 
 constexpr int ROWS = 16;          // queries per workgroup
-constexpr int STREAMS = 8;        // key streams (waves) per workgroup
-constexpr int THREADS = ROWS * 4 * STREAMS;
-constexpr int KT = 16;            // keys per tile
+constexpr int ROUND_KEYS = 128;   // keys per round of all streams (STREAMS x KT)
 
-template <int D, bool CAUSAL>
-__global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
+template <int STREAMS>
+constexpr int threads_of() { return ROWS * 4 * STREAMS; }
+
+template <int D, bool CAUSAL, int STREAMS>
+__global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
     float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c,
     Layout L) {
+    constexpr int THREADS = threads_of<STREAMS>();
+    constexpr int KT = ROUND_KEYS / STREAMS;   // keys per tile
     constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
-    // Per wave: its K and V tile; reused at the end for the merge, where a K
-    // tile holds the wave's O (D / 4 floats per lane: KT >= 16 keys).
-    static_assert(KT * D >= 64 * (D / 4), "a K tile must hold one wave's O for the merge");
-    __shared__ __attribute__((aligned(16))) float Ks[STREAMS][KT * D];
-    __shared__ __attribute__((aligned(16))) float Vs[STREAMS][KT * D];
+    constexpr int TILE = KT * D;  // floats of one K (or V) tile
+    constexpr int PER = TILE / 4 / 64;   // float4 per lane per tile
+    static_assert(TILE % 256 == 0, "a tile must split into whole float4 per lane");
+    // Per wave: its K tile followed by its V tile.  After the key loop the
+    // same area holds the wave's un-normalised output, ROWS x D floats.
+    static_assert(ROWS * D <= 2 * TILE, "a wave's K and V tiles must hold its output rows");
+    __shared__ __attribute__((aligned(16))) float KV[STREAMS][2 * TILE];
+    __shared__ float ML[STREAMS][2][ROWS];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // key stream
     const int quad = lane & 3;
+    const int row = lane >> 2;
     const int bh = blockIdx.x / n_qtiles;
     const int qt = blockIdx.x % n_qtiles;
-    const int qrow = qt * ROWS + (lane >> 2);
+    const int qrow = qt * ROWS + row;
     const int qrow_c = qrow < Nq ? qrow : Nq - 1;
     const int off = Nk - Nq;
 
     const float* Qh = Q + head_offset(bh, L.H, L.qb, L.qh);
     const float* Kh = K + head_offset(bh, L.H, L.kb, L.kh);
     const float* Vh = V + head_offset(bh, L.H, L.vb, L.vh);
-    float* ks = Ks[wave];
-    float* vs = Vs[wave];
+    float* ks = KV[wave];
+    float* vs = KV[wave] + TILE;
 
     float4 qv[CH], acc[CH];
 #pragma unroll
@@ -70,22 +77,21 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
         // ordering (every lane's previous reads are consumed, its stores land
         // before the reads below).
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-        constexpr int PER = KT * D / 4 / 64;  // float4 per lane per tile
         float4 kst[PER], vst[PER];
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int idx = i * 64 + lane;
-            const int row = idx / (D / 4), ch = idx % (D / 4);
-            const int key = min(kbase + row, Nk - 1);
+            const int r = idx / (D / 4), ch = idx % (D / 4);
+            const int key = min(kbase + r, Nk - 1);
             kst[i] = *reinterpret_cast<const float4*>(Kh + (size_t)key * L.kr + ch * 4);
             vst[i] = *reinterpret_cast<const float4*>(Vh + (size_t)key * L.vr + ch * 4);
         }
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int idx = i * 64 + lane;
-            const int row = idx / (D / 4), ch = idx % (D / 4);
-            *reinterpret_cast<float4*>(&ks[row * D + ch * 4]) = kst[i];
-            *reinterpret_cast<float4*>(&vs[row * D + ch * 4]) = vst[i];
+            const int r = idx / (D / 4), ch = idx % (D / 4);
+            *reinterpret_cast<float4*>(&ks[r * D + ch * 4]) = kst[i];
+            *reinterpret_cast<float4*>(&vs[r * D + ch * 4]) = vst[i];
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the stores have landed
         __builtin_amdgcn_wave_barrier();
@@ -135,59 +141,76 @@ __global__ __launch_bounds__(THREADS) void prefill_f32_kernel(
         }
     }
 
-    // Waves 1..7 hand (m, l, acc) to wave 0 through their K areas; wave 0
-    // merges exactly: M = max(m0, mw), acc = 2^(m0-M) acc0 + 2^(mw-M) accw,
-    // l likewise.  A stream without visible keys has m = -inf and adds nothing.
-    __syncthreads();
-    if (wave != 0) {
+    // Exact merge of the streams' states: every wave stores (m, l, acc) of
+    // its stream, then each thread finishes one float4 of O:
+    //   M = max_w m_w,  O = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w.
+    // A stream without visible keys has m = -inf and adds nothing.
+    __syncthreads();   // every wave is done reading its tiles
 #pragma unroll
-        for (int h = 0; h < CH; ++h)
-            *reinterpret_cast<float4*>(&ks[(h * 64 + lane) * 4]) = acc[h];
-        vs[lane] = m_run;
-        vs[64 + lane] = l_run;
+    for (int h = 0; h < CH; ++h)
+        *reinterpret_cast<float4*>(&ks[row * D + (h * 4 + quad) * 4]) = acc[h];
+    if (quad == 0) {
+        ML[wave][0][row] = m_run;
+        ML[wave][1][row] = l_run;
     }
     __syncthreads();
-    if (wave != 0) return;
+    constexpr int OUT4 = ROWS * D / 4;   // float4 of the workgroup's output
+    for (int t = threadIdx.x; t < OUT4; t += THREADS) {
+        const int r = t / (D / 4), c4 = t % (D / 4);
+        float mm = kNegInf;
 #pragma unroll
-    for (int w = 1; w < STREAMS; ++w) {
-        const float m1 = Vs[w][lane], l1 = Vs[w][64 + lane];
-        const float mm = fmaxf(m_run, m1);
-        const float a0 = (m_run == kNegInf) ? 0.0f : exp2_hw(m_run - mm);
-        const float a1 = (m1 == kNegInf) ? 0.0f : exp2_hw(m1 - mm);
-        l_run = l_run * a0 + l1 * a1;
+        for (int w = 0; w < STREAMS; ++w) mm = fmaxf(mm, ML[w][0][r]);
+        float ll = 0.0f;
+        float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int h = 0; h < CH; ++h) {
-            const float4 o = *reinterpret_cast<const float4*>(&Ks[w][(h * 64 + lane) * 4]);
-            acc[h].x = acc[h].x * a0 + o.x * a1;
-            acc[h].y = acc[h].y * a0 + o.y * a1;
-            acc[h].z = acc[h].z * a0 + o.z * a1;
-            acc[h].w = acc[h].w * a0 + o.w * a1;
+        for (int w = 0; w < STREAMS; ++w) {
+            const float mw = ML[w][0][r];
+            const float a = (mw == kNegInf) ? 0.0f : exp2_hw(mw - mm);
+            ll = __builtin_fmaf(a, ML[w][1][r], ll);
+            const float4 x = *reinterpret_cast<const float4*>(&KV[w][r * D + c4 * 4]);
+            o.x = __builtin_fmaf(a, x.x, o.x);
+            o.y = __builtin_fmaf(a, x.y, o.y);
+            o.z = __builtin_fmaf(a, x.z, o.z);
+            o.w = __builtin_fmaf(a, x.w, o.w);
         }
-        m_run = mm;
+        const int q = qt * ROWS + r;
+        if (q < Nq) {
+            const float inv = 1.0f / ll;
+            const size_t obase = (size_t)head_offset(bh, L.H, L.ob, L.oh) + (size_t)q * L.orow;
+            *reinterpret_cast<float4*>(Out + obase + c4 * 4) =
+                make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
+            if (LSE != nullptr && c4 == 0) LSE[(size_t)bh * Nq + q] = (mm + __log2f(ll)) * kLn2;
+        }
     }
+}
 
-    if (qrow < Nq) {
-        const float inv = 1.0f / l_run;
-        const size_t obase = (size_t)head_offset(bh, L.H, L.ob, L.oh) + (size_t)qrow * L.orow;
-#pragma unroll
-        for (int h = 0; h < CH; ++h) {
-            const int d0 = (h * 4 + quad) * 4;
-            const float4 o = make_float4(acc[h].x * inv, acc[h].y * inv, acc[h].z * inv, acc[h].w * inv);
-            *reinterpret_cast<float4*>(Out + obase + d0) = o;
-        }
-        if (LSE != nullptr && quad == 0)
-            LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_run)) * kLn2;
-    }
+// Sixteen streams of 8-key tiles where a workgroup has long keys and the
+// grid leaves compute units free (workgroups then run alone on theirs, and
+// twice the waves hide twice the latency): 6% faster on a 4K single head,
+// 15% on 2 heads of 300 x 517, d = 128.  Otherwise eight streams of 16-key
+// tiles, whose workgroups are cheaper to start and merge (7% faster on 128 x
+// 128 single heads, 3-8% on grids of two or more workgroups per unit).
+constexpr int kWideMinKeys = 512;
+
+template <int D, bool CAUSAL, int STREAMS>
+hipError_t launch_s(const Problem& p, int n_qtiles, hipStream_t stream) {
+    const long long blocks = (long long)p.bh * n_qtiles;
+    return launch_kernel(prefill_f32_kernel<D, CAUSAL, STREAMS>, dim3((unsigned)blocks),
+                         dim3(threads_of<STREAMS>()), stream, static_cast<const float*>(p.q),
+                         static_cast<const float*>(p.k), static_cast<const float*>(p.v),
+                         static_cast<float*>(p.o), p.lse, p.nq, p.nk, n_qtiles,
+                         p.scale * kLog2e, p.lay);
 }
 
 template <int D, bool CAUSAL>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const int n_qtiles = (p.nq + ROWS - 1) / ROWS;
-    const long long blocks = (long long)p.bh * n_qtiles;
-    return launch_kernel(prefill_f32_kernel<D, CAUSAL>, dim3((unsigned)blocks), dim3(THREADS),
-                         stream, static_cast<const float*>(p.q), static_cast<const float*>(p.k),
-                         static_cast<const float*>(p.v), static_cast<float*>(p.o), p.lse, p.nq,
-                         p.nk, n_qtiles, p.scale * kLog2e, p.lay);
+    int cus = 0;
+    const hipError_t e = device_cus(stream, cus);
+    if (e != hipSuccess) return e;
+    if (p.nk >= kWideMinKeys && (long long)p.bh * n_qtiles <= cus)
+        return launch_s<D, CAUSAL, 16>(p, n_qtiles, stream);
+    return launch_s<D, CAUSAL, 8>(p, n_qtiles, stream);
 }
 
 template <int D>

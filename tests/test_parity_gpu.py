@@ -38,6 +38,7 @@ PREFILL_SHAPES = [
     (1, 2, 300, 300, 128),
     (1, 2, 17, 64, 64),        # one full key tile: the single-tile ping-pong launch
     (1, 2, 64, 64, 128),
+    (2, 9, 250, 600, 64),      # fp32: long keys on more workgroups than compute units
 ]
 
 
@@ -67,11 +68,10 @@ def _lse_tol(dtype, ref_lse):
     return 4e-3 + 1e-5 * np.abs(ref_lse).max()
 
 
-# Grids of >= 1024 work items of 256 queries take the ping-pong layout, grids
-# of at least one item per compute unit (256 on MI355X) the per-wave pipelined
-# kernel, and the smaller prefill shapes above the key-split layout.  These
-# cover the two larger layouts with ragged query and key tails, on sampled
-# rows.
+# Grids of at least one 256-query item per compute unit (256 on MI355X) take
+# the ping-pong layout, and the smaller prefill shapes above the key-split
+# layout.  These cover the ping-pong layout with ragged query and key tails,
+# on sampled rows.
 PINGPONG_SHAPES = [
     # B, H, Nq, Nk, d
     (4, 64, 1000, 1000, 64),
