@@ -5,25 +5,7 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
-#include <atomic>
-
 namespace moa {
-
-// Compute units of the device that runs `stream` (cached per device).
-inline hipError_t device_cus(hipStream_t stream, int& cus) {
-    constexpr int kMaxDevices = 64;
-    static std::atomic<int> cache[kMaxDevices];
-    hipDevice_t dev = 0;
-    hipError_t e = hipStreamGetDevice(stream, &dev);
-    if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < kMaxDevices && (cus = cache[dev].load(std::memory_order_relaxed)) > 0)
-        return hipSuccess;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
-    if (cus < 1) cus = 1;
-    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(cus, std::memory_order_relaxed);
-    return hipSuccess;
-}
 
 // Element strides of Q, K, V and O over batch and head (64-bit) and over
 // rows (32-bit); the d dimension of every tensor is contiguous.  Contiguous

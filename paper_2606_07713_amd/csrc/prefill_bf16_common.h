@@ -1,7 +1,9 @@
 // Pieces shared by the bf16 prefill kernels: LDS tile layout (swizzle and the
-// O^T row order) and the persistent work schedule.
+// O^T row order), the persistent work schedule and the device query that
+// sizes a persistent grid.
 #pragma once
 
+#include <atomic>
 #include <stdint.h>
 
 #include "device_common.h"
@@ -141,6 +143,22 @@ __device__ __forceinline__ void barrier_no_fence() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Compute units of the device that runs `stream` (cached per device).
+inline hipError_t device_cus(hipStream_t stream, int& cus) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices];
+    hipDevice_t dev = 0;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < kMaxDevices && (cus = cache[dev].load(std::memory_order_relaxed)) > 0)
+        return hipSuccess;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    if (cus < 1) cus = 1;
+    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(cus, std::memory_order_relaxed);
+    return hipSuccess;
 }
 
 }  // namespace pf

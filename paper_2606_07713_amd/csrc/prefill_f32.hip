@@ -16,6 +16,7 @@
 // output_dnf); only O (and optional LSE) are written.
 #include "device_common.h"
 #include "launch.h"
+#include "prefill_bf16_common.h"   // device_cus
 
 namespace moa {
 namespace {
@@ -206,7 +207,7 @@ template <int D, bool CAUSAL>
 hipError_t launch(const Problem& p, hipStream_t stream) {
     const int n_qtiles = (p.nq + ROWS - 1) / ROWS;
     int cus = 0;
-    const hipError_t e = device_cus(stream, cus);
+    const hipError_t e = pf::device_cus(stream, cus);
     if (e != hipSuccess) return e;
     if (p.nk >= kWideMinKeys && (long long)p.bh * n_qtiles <= cus)
         return launch_s<D, CAUSAL, 16>(p, n_qtiles, stream);
