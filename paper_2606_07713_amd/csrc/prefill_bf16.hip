@@ -479,7 +479,56 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     if (!KSPLIT || grp == 0) {
     const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
-    if (qrow < Nq) {
+    if constexpr (OUT_BF16) {
+        // In the O^T accumulator layout a lane holds 8-byte pieces of one
+        // query row, so a direct store would write 32 rows per instruction.
+        // The wave first puts its 32 rows into LDS in row order, then stores
+        // whole rows: 16 bytes per lane, 64 / CHUNKS rows per instruction.
+        // Its staging area (32 rows, 16-byte chunks XOR-swizzled by row) is
+        // a slice of the tile stages no wave reads any more: the ping-pong
+        // layout's four stages hold two waves each; in the key split each
+        // wave reuses the area it read its partner's state from.
+        unsigned char* stg;
+        if constexpr (KSPLIT) {
+            stg = (qw < 2 ? k_st0 : k_st1) + (qw & 1) * (D / 2) * 64 * sizeof(float);
+        } else {
+            unsigned char* st = (qw < 2) ? k_st0 : (qw < 4) ? k_st1 : (qw < 6) ? v_st0 : v_st1;
+            stg = st + (qw & 1) * 32 * RB;
+        }
+        constexpr int CHK = C::CHUNKS;
+        // The lane index goes through an empty asm so that these addresses
+        // are formed here: hoisted out of the item loop they would hold ~24
+        // registers through the key loop and cost its LDS read-ahead.
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int cl = ln & 31, hf = ln >> 5;
+#pragma unroll
+        for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int dv = dv_of<D>(b, g * 8 + hf * 4);
+                const uint2 w = make_uint2(pack_bf16x2(oacc[b][g * 4 + 0] * inv, oacc[b][g * 4 + 1] * inv),
+                                           pack_bf16x2(oacc[b][g * 4 + 2] * inv, oacc[b][g * 4 + 3] * inv));
+                const uint32_t a = (uint32_t)cl * RB +
+                                   (uint32_t)((((dv >> 3) ^ (cl & (CHK - 1))) * 16) + (dv & 7) * 2);
+                *reinterpret_cast<uint2*>(stg + a) = w;
+            }
+        wait_lgkmcnt0();   // this wave's rows are in LDS (only this wave reads them)
+        constexpr int RPI = 64 / CHK;   // rows per store instruction
+        const int rr = ln / CHK, ch = ln % CHK;
+#pragma unroll
+        for (int i = 0; i < 32 / RPI; ++i) {
+            const int r = i * RPI + rr;
+            const uint4 v = *reinterpret_cast<const uint4*>(
+                stg + (uint32_t)r * RB + (uint32_t)((ch ^ (r & (CHK - 1))) * 16));
+            const int q = wave_q_first + r;
+            if (q < Nq)
+                *reinterpret_cast<uint4*>(static_cast<u16*>(Out) + (size_t)A.o_head(bh) +
+                                          (size_t)q * A.orow() + ch * 8) = v;
+        }
+        if (LSE != nullptr && half == 0 && qrow < Nq)
+            LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
+    } else if (qrow < Nq) {
         const size_t obase = (size_t)A.o_head(bh) + (size_t)qrow * A.orow();
 #pragma unroll
         for (int b = 0; b < D / 32; ++b) {
@@ -488,13 +537,8 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
                 const int dv = dv_of<D>(b, g * 8 + half * 4);
                 const float o0 = oacc[b][g * 4 + 0] * inv, o1 = oacc[b][g * 4 + 1] * inv;
                 const float o2 = oacc[b][g * 4 + 2] * inv, o3 = oacc[b][g * 4 + 3] * inv;
-                if (OUT_BF16) {
-                    uint2 w = make_uint2(pack_bf16x2(o0, o1), pack_bf16x2(o2, o3));
-                    *reinterpret_cast<uint2*>(static_cast<u16*>(Out) + obase + dv) = w;
-                } else {
-                    *reinterpret_cast<float4*>(static_cast<float*>(Out) + obase + dv) =
-                        make_float4(o0, o1, o2, o3);
-                }
+                *reinterpret_cast<float4*>(static_cast<float*>(Out) + obase + dv) =
+                    make_float4(o0, o1, o2, o3);
             }
         }
         if (LSE != nullptr && half == 0)
@@ -503,8 +547,13 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     }
     }
     // Every wave is done with this item's LDS before the next item's first
-    // tile load lands there.
-    __syncthreads();
+    // tile loads land there: its LDS reads have returned (their values are
+    // consumed above; the wait makes it explicit), and the barrier orders
+    // them before any wave's next loads.  No memory fence: it would wait for
+    // the O stores just issued (vmcnt counts stores too), which nothing in
+    // this workgroup reads.
+    wait_lgkmcnt0();
+    barrier_no_fence();
     }
 }
 
