@@ -491,26 +491,75 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
         }
     }
 
+    // ---- Output rows.  In the O^T accumulator layout a lane holds pieces of
+    // one query row, so a direct store would write 32 rows per instruction.
+    // A wave first puts its 32 rows into LDS in row order (16-byte chunks
+    // XOR-swizzled by row), then stores whole rows, 16 bytes per lane.  Its
+    // staging area (32 rows of 2*D bytes) is a slice of the tile stages that
+    // no wave reads any more: the ping-pong layout's four stages hold two
+    // waves each; in the key split each wave of group 0 reuses the area it
+    // read its partner's state from.  The lane index goes through an empty
+    // asm so that the staging addresses are formed here: hoisted out of the
+    // item loop they would hold ~24 registers through the key loop and cost
+    // its LDS read-ahead.
+    unsigned char* stg;
+    if constexpr (KSPLIT) {
+        stg = (qw < 2 ? k_st0 : k_st1) + (qw & 1) * (D / 2) * 64 * sizeof(float);
+    } else {
+        unsigned char* st = (qw < 2) ? k_st0 : (qw < 4) ? k_st1 : (qw < 6) ? v_st0 : v_st1;
+        stg = st + (qw & 1) * 32 * RB;
+    }
+    // fp32 rows (the split-K partial state or fp32 O), times `scl`, in two
+    // passes of D/2 columns: row_ptr(r) is the destination of row r of the
+    // wave's 32, or null for rows past Nq.
+    auto store_rows_f32 = [&](float scl, auto row_ptr) {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int cl = ln & 31, hf = ln >> 5;
+        constexpr int HB = D * 2;       // bytes of a half row (D/2 floats)
+        constexpr int HCH = HB / 16;    // its 16-byte chunks
+        constexpr int RPI = 64 / HCH;   // rows per store instruction
+        const int rr = ln / HCH, ch = ln % HCH;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    if (dv_of<D>(b, g * 8) / (D / 2) != h) continue;
+                    const int c = (dv_of<D>(b, g * 8 + hf * 4) - h * (D / 2)) / 4;
+                    *reinterpret_cast<float4*>(stg + (uint32_t)cl * HB +
+                                               (uint32_t)((c ^ (cl & (HCH - 1))) * 16)) =
+                        make_float4(oacc[b][g * 4 + 0] * scl, oacc[b][g * 4 + 1] * scl,
+                                    oacc[b][g * 4 + 2] * scl, oacc[b][g * 4 + 3] * scl);
+                }
+            wait_lgkmcnt0();   // this wave's rows are in LDS (only this wave reads them)
+#pragma unroll
+            for (int i = 0; i < 32 / RPI; ++i) {
+                const int r = i * RPI + rr;
+                const float4 v = *reinterpret_cast<const float4*>(
+                    stg + (uint32_t)r * HB + (uint32_t)((ch ^ (r & (HCH - 1))) * 16));
+                float* dst = row_ptr(r);
+                if (dst != nullptr) *reinterpret_cast<float4*>(dst + h * (D / 2) + ch * 4) = v;
+            }
+        }
+    };
+
     // ---- a8 (split-K): the partial state of this key share, un-normalised,
     // for the combine pass.
     if constexpr (PARTIAL) {
     if (grp == 0) {
-    const float l_tot = half_sum(l_run);
-    if (qrow < Nq) {
-        const size_t prow = ((size_t)bh * Nq + qrow) * n_splits + split;
-        float* acc_out = static_cast<float*>(Out) + prow * D;
-#pragma unroll
-        for (int b = 0; b < D / 32; ++b)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                *reinterpret_cast<float4*>(acc_out + dv_of<D>(b, g * 8 + half * 4)) =
-                    make_float4(oacc[b][g * 4 + 0], oacc[b][g * 4 + 1], oacc[b][g * 4 + 2],
-                                oacc[b][g * 4 + 3]);
-        if (half == 0) {
+        const float l_tot = half_sum(l_run);
+        store_rows_f32(1.0f, [&](int r) -> float* {
+            const int q = wave_q_first + r;
+            return q < Nq ? static_cast<float*>(Out) + (((size_t)bh * Nq + q) * n_splits + split) * D
+                          : nullptr;
+        });
+        if (qrow < Nq && half == 0) {
+            const size_t prow = ((size_t)bh * Nq + qrow) * n_splits + split;
             LSE[prow * 2 + 0] = m_run;
             LSE[prow * 2 + 1] = l_tot;
         }
-    }
     }
     } else {
     // ---- a7: epilogue, O = acc / l: the only device-memory write (key
@@ -519,25 +568,7 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
     const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
     if constexpr (OUT_BF16) {
-        // In the O^T accumulator layout a lane holds 8-byte pieces of one
-        // query row, so a direct store would write 32 rows per instruction.
-        // The wave first puts its 32 rows into LDS in row order, then stores
-        // whole rows: 16 bytes per lane, 64 / CHUNKS rows per instruction.
-        // Its staging area (32 rows, 16-byte chunks XOR-swizzled by row) is
-        // a slice of the tile stages no wave reads any more: the ping-pong
-        // layout's four stages hold two waves each; in the key split each
-        // wave reuses the area it read its partner's state from.
-        unsigned char* stg;
-        if constexpr (KSPLIT) {
-            stg = (qw < 2 ? k_st0 : k_st1) + (qw & 1) * (D / 2) * 64 * sizeof(float);
-        } else {
-            unsigned char* st = (qw < 2) ? k_st0 : (qw < 4) ? k_st1 : (qw < 6) ? v_st0 : v_st1;
-            stg = st + (qw & 1) * 32 * RB;
-        }
         constexpr int CHK = C::CHUNKS;
-        // The lane index goes through an empty asm so that these addresses
-        // are formed here: hoisted out of the item loop they would hold ~24
-        // registers through the key loop and cost its LDS read-ahead.
         int ln = lane;
         asm volatile("" : "+v"(ln));
         const int cl = ln & 31, hf = ln >> 5;
@@ -565,24 +596,15 @@ __global__ __launch_bounds__(THREADS, 1) void prefill_bf16_kernel(
                 *reinterpret_cast<uint4*>(static_cast<u16*>(Out) + (size_t)A.o_head(bh) +
                                           (size_t)q * A.orow() + ch * 8) = v;
         }
-        if (LSE != nullptr && half == 0 && qrow < Nq)
-            LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
-    } else if (qrow < Nq) {
-        const size_t obase = (size_t)A.o_head(bh) + (size_t)qrow * A.orow();
-#pragma unroll
-        for (int b = 0; b < D / 32; ++b) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int dv = dv_of<D>(b, g * 8 + half * 4);
-                const float o0 = oacc[b][g * 4 + 0] * inv, o1 = oacc[b][g * 4 + 1] * inv;
-                const float o2 = oacc[b][g * 4 + 2] * inv, o3 = oacc[b][g * 4 + 3] * inv;
-                *reinterpret_cast<float4*>(static_cast<float*>(Out) + obase + dv) =
-                    make_float4(o0, o1, o2, o3);
-            }
-        }
-        if (LSE != nullptr && half == 0)
-            LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
+    } else {
+        store_rows_f32(inv, [&](int r) -> float* {
+            const int q = wave_q_first + r;
+            return q < Nq ? static_cast<float*>(Out) + (size_t)A.o_head(bh) + (size_t)q * A.orow()
+                          : nullptr;
+        });
     }
+    if (LSE != nullptr && half == 0 && qrow < Nq)
+        LSE[(size_t)bh * Nq + qrow] = (m_run + __log2f(l_tot)) * kLn2;
     }
     }
     // Every wave is done with this item's LDS before the next item's first
