@@ -1,8 +1,8 @@
 """Strided layouts on the GPU (moa_attn_fwd_strided through attn_fwd): the same
 seeded inputs stored as [B, N, H, d] views, packed QKV buffers, padded rows and
 K/V shared by every head, against the oracle on the contiguous arrays.  Every
-kernel family is covered: the three bf16 prefill layouts (chosen by the number
-of 256-query work items), fp32 prefill and decode.  The layouts are the
+kernel family is covered: the two bf16 prefill layouts (ping-pong on a large
+and on a mid-size grid, key split on a small one), fp32 prefill and decode.  The layouts are the
 storage functions of the footnote to eq. gamma with per-dimension strides.
 
 Layouts with a strided head dimension -- column-major heads ([B][H][d][N]),
@@ -106,8 +106,7 @@ def _inputs(B, H, Nq, Nk, d, dtype, layout, seed):
 # (B, H, Nq, Nk, d, dtype): kernel family each exercises
 SHAPES = {
     "pingpong": (2, 128, 1000, 1000, 64, "bf16"),    # 1024 items of 256 queries
-    "pipelined": (1, 128, 600, 600, 128, "bf16"),    # 384 items (non-causal: causal d = 128 grids
-                                                     # of this size take the ping-pong layout)
+    "pingpong_mid": (1, 128, 600, 600, 128, "bf16"), # 384 items: 1.5 per compute unit
     "keysplit": (2, 4, 300, 300, 128, "bf16"),       # 16 items
     "f32": (2, 3, 100, 100, 64, "f32"),
     "decode": (4, 8, 1, 3000, 128, "bf16"),
@@ -140,7 +139,7 @@ def test_strided_inputs_match_oracle(family, layout):
 def test_strided_output_bshd(family):
     """O written into a [B, N, H, d] buffer; every element is written (NaN-filled first)."""
     B, H, Nq, Nk, d, dtype = SHAPES[family]
-    causal = family not in ("decode", "pipelined")
+    causal = family not in ("decode", "pingpong_mid")
     q, k, v = gen(B, H, Nq, Nk, d, dtype, _seed("out", family))
     o = _run(q, k, v, "bshd", out_layout="bshd", causal=causal)
     assert not np.isnan(o).any()
@@ -156,7 +155,7 @@ def test_strided_output_bshd(family):
 def test_gathered_inputs_match_oracle(family, layout):
     """Strided head dimensions and unaligned rows (moa_attn_fwd_onf's gather kernel)."""
     B, H, Nq, Nk, d, dtype = SHAPES[family]
-    causal = family in ("pipelined", "keysplit", "decode")
+    causal = family in ("pingpong_mid", "keysplit", "decode")
     say(f"gathered layout {layout} family {family} {SHAPES[family]} causal={causal}")
     q, k, v = gen(B, H, Nq, Nk, d, dtype, _seed("gather", family, layout))
     for out_dtype in dict.fromkeys((dtype, "f32")):
@@ -190,7 +189,7 @@ def test_gathered_output_colmajor(family):
 
 def test_strided_equals_contiguous_bitwise():
     """The same values in two storages give bit-identical outputs (no layout-dependent math)."""
-    B, H, Nq, Nk, d, dtype = SHAPES["pipelined"]
+    B, H, Nq, Nk, d, dtype = SHAPES["pingpong_mid"]
     q, k, v = gen(B, H, Nq, Nk, d, dtype, _seed("bits"))
     a = _run(q, k, v, "contiguous", causal=False)
     b = _run(q, k, v, "bshd", causal=False)
