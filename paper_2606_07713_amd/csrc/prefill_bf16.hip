@@ -22,7 +22,10 @@
 // (buffer_load ... lds, 16 bytes per lane, no register staging) through
 // two-stage rings; rows past Nk come back as zeros from the buffer bounds.
 // LDS rows are stored with a 16-byte-chunk XOR swizzle instead of padding,
-// because direct-to-LDS writes are contiguous per instruction.
+// because direct-to-LDS writes are contiguous per instruction.  The output
+// (and, in the key-split layout, the Q tile) also passes through LDS, so that
+// device memory is written (read) in whole rows rather than in the 8- or
+// 16-byte pieces per row that the MFMA register layouts hold.
 //
 // Ping-pong.  Waves w and w + 4 share a SIMD.  The workgroup advances in
 // phases separated by barriers; in each phase one group of four waves issues
@@ -32,12 +35,14 @@
 // ALU of every SIMD busy at the same time.
 //
 // Softmax.  Scores are kept in raw units; with c = scale * log2(e) the weight
-// of key j is 2^(s_j c - m) where m is a running row maximum in log2 units.
-// The reference maximum is raised (and O, l rescaled) only when a tile exceeds
-// it by more than kRescaleSlack; otherwise weights up to 2^kRescaleSlack are
-// accumulated against the stale maximum.  The final O = acc / l uses the same
-// reference for numerator and denominator, so the result is the same softmax
-// (Steps I-IV regrouped over key tiles).
+// of key j is 2^(s_j c - m) where m is a running reference (log2 units) in
+// place of the row maximum.  A tile's weights are first formed against the
+// current reference without computing the tile max; only when their partial
+// sum exceeds kFastSumLimit (or overflows) is the reference raised, to
+// kRefHeadroom above the tile max (and O, l rescaled), and the tile redone.
+// The final O = acc / l uses the same reference for numerator and
+// denominator, so any reference gives the same quotient: the softmax of
+// Steps I-IV regrouped over key tiles.
 #include <algorithm>
 #include <type_traits>
 
@@ -61,8 +66,8 @@ __device__ __forceinline__ void wait_loads_to_lds() {
 // KSPLIT = true: 4 query blocks x 2 key halves = 128 queries per workgroup;
 //   group g streams key tiles of its half through its own LDS rings (both
 //   groups in the same phase), and group 1 hands its softmax state (m, l, O)
-//   to group 0 through LDS at the end for an exact merge.  Used when the
-//   ping-pong grid is too small to fill the GPU.
+//   to group 0 through LDS at the end for an exact merge.  Used for grids
+//   the ping-pong layout would leave partly idle (see use_key_split).
 // PARTIAL = true (with KSPLIT): split-K across workgroups for grids smaller
 //   still.  Work item = (batch*head, query tile, key split s of n_splits):
 //   the item covers the s-th of n_splits equal shares of the query tile's
