@@ -3,17 +3,17 @@
 //
 // Used where the inputs are fp32 and the result must stay within fp32
 // rounding of the exact attention (no bf16 rounding of any operand).  One
-// workgroup owns 16 queries of one (batch*head); each query row is handled by
-// a quad of 4 lanes that split d.  The waves of a workgroup (8, or 16 for long
-// keys on small grids) hold the same queries and walk disjoint key streams
-// (wave w takes tiles w, w + STREAMS, ...; 128 keys per round of the
-// workgroup), each staging its own K/V tiles in its own LDS area, read by its
-// quads as broadcasts.  At the end every wave stores its softmax state and all
-// threads merge the streams exactly, one float4 of O each.  The key split
-// keeps each wave's chain of dependent loads and vector instructions short,
-// which is what these small problems are bound by.  Scores, the running max
-// and sum and the exponentials stay in registers (DNF eqs. dnf_attn /
-// output_dnf); only O (and optional LSE) are written.
+// workgroup owns a tile of query rows of one (batch*head); each row is
+// handled by QL lanes that split d (4 or 8).  The waves of a workgroup hold
+// the same rows and walk disjoint key streams (wave w takes tiles w,
+// w + STREAMS, ...; 128 keys per round of the workgroup), each staging its
+// own K/V tiles in its own LDS area, read by its lanes as broadcasts.  At the
+// end every wave stores its softmax state and all threads merge the streams
+// exactly, one float4 of O each.  The key split keeps each wave's chain of
+// dependent loads and vector instructions short, which is what these small
+// problems are bound by.  Scores, the running max and sum and the
+// exponentials stay in registers (DNF eqs. dnf_attn / output_dnf); only O
+// (and optional LSE) are written.
 #include "device_common.h"
 #include "launch.h"
 #include "prefill_bf16_common.h"   // device_cus
@@ -21,20 +21,24 @@
 namespace moa {
 namespace {
 
-constexpr int ROWS = 16;          // queries per workgroup
 constexpr int ROUND_KEYS = 128;   // keys per round of all streams (STREAMS x KT)
 
+// QL lanes share a query row (they split d); a wave holds 64 / QL rows, and
+// every wave of a workgroup holds the same rows.
+template <int QL>
+constexpr int rows_of() { return 64 / QL; }
 template <int STREAMS>
-constexpr int threads_of() { return ROWS * 4 * STREAMS; }
+constexpr int threads_of() { return 64 * STREAMS; }
 
-template <int D, bool CAUSAL, int STREAMS>
+template <int D, bool CAUSAL, int STREAMS, int QL>
 __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
     float* __restrict__ Out, float* __restrict__ LSE, int Nq, int Nk, int n_qtiles, float c,
     Layout L) {
     constexpr int THREADS = threads_of<STREAMS>();
+    constexpr int ROWS = rows_of<QL>();
     constexpr int KT = ROUND_KEYS / STREAMS;   // keys per tile
-    constexpr int CH = D / 16;    // float4 chunks per lane (chunk j*4 + quad)
+    constexpr int CH = D / (4 * QL);   // float4 chunks per lane (chunk j*QL + quad)
     constexpr int TILE = KT * D;  // floats of one K (or V) tile
     constexpr int PER = TILE / 4 / 64;   // float4 per lane per tile
     static_assert(TILE % 256 == 0, "a tile must split into whole float4 per lane");
@@ -46,8 +50,8 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // key stream
-    const int quad = lane & 3;
-    const int row = lane >> 2;
+    const int quad = lane % QL;   // this lane's part of the row
+    const int row = lane / QL;
     const int bh = blockIdx.x / n_qtiles;
     const int qt = blockIdx.x % n_qtiles;
     const int qrow = qt * ROWS + row;
@@ -63,7 +67,7 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     float4 qv[CH], acc[CH];
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
-        qv[j] = *reinterpret_cast<const float4*>(Qh + (size_t)qrow_c * L.qr + (j * 4 + quad) * 4);
+        qv[j] = *reinterpret_cast<const float4*>(Qh + (size_t)qrow_c * L.qr + (j * QL + quad) * 4);
         acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     float m_run = kNegInf, l_run = 0.0f;
@@ -105,13 +109,13 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
             float part = 0.0f;
 #pragma unroll
             for (int h = 0; h < CH; ++h) {
-                const float4 kk = *reinterpret_cast<const float4*>(&ks[j * D + (h * 4 + quad) * 4]);
+                const float4 kk = *reinterpret_cast<const float4*>(&ks[j * D + (h * QL + quad) * 4]);
                 part = __builtin_fmaf(qv[h].x, kk.x, part);
                 part = __builtin_fmaf(qv[h].y, kk.y, part);
                 part = __builtin_fmaf(qv[h].z, kk.z, part);
                 part = __builtin_fmaf(qv[h].w, kk.w, part);
             }
-            const float s = group_sum<4>(part);
+            const float s = group_sum<QL>(part);
             const int key = kbase + j;
             const bool vis = key < Nk && (!CAUSAL || key <= qrow + off);
             t[j] = vis ? s * c : kNegInf;
@@ -133,7 +137,7 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
             l_run += p;
 #pragma unroll
             for (int h = 0; h < CH; ++h) {
-                const float4 vv = *reinterpret_cast<const float4*>(&vs[j * D + (h * 4 + quad) * 4]);
+                const float4 vv = *reinterpret_cast<const float4*>(&vs[j * D + (h * QL + quad) * 4]);
                 acc[h].x = __builtin_fmaf(p, vv.x, acc[h].x);
                 acc[h].y = __builtin_fmaf(p, vv.y, acc[h].y);
                 acc[h].z = __builtin_fmaf(p, vv.z, acc[h].z);
@@ -149,7 +153,7 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     __syncthreads();   // every wave is done reading its tiles
 #pragma unroll
     for (int h = 0; h < CH; ++h)
-        *reinterpret_cast<float4*>(&ks[row * D + (h * 4 + quad) * 4]) = acc[h];
+        *reinterpret_cast<float4*>(&ks[row * D + (h * QL + quad) * 4]) = acc[h];
     if (quad == 0) {
         ML[wave][0][row] = m_run;
         ML[wave][1][row] = l_run;
@@ -185,18 +189,31 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     }
 }
 
-// Sixteen streams of 8-key tiles where a workgroup has long keys and the
-// grid leaves compute units free (workgroups then run alone on theirs, and
-// twice the waves hide twice the latency): 6% faster on a 4K single head,
-// 15% on 2 heads of 300 x 517, d = 128.  Otherwise eight streams of 16-key
-// tiles, whose workgroups are cheaper to start and merge (7% faster on 128 x
-// 128 single heads, 3-8% on grids of two or more workgroups per unit).
+// Three shapes of workgroup, by grid size (raw C-ABI calls, us, one box):
+//
+//   shape (streams x key tile, lanes per row, rows)   8x16, 4, 16   16x8, 4, 16   16x8, 8, 8
+//   B1 H1 128 x 128, d = 64                            6.39          6.83          4.97
+//   B1 H1 128 x 128, d = 128                           9.73          10.27         6.73
+//   B1 H2 300 x 517, d = 128                           31.7          27.9          17.2
+//   B1 H1 2K x 2K causal, d = 128                      103.1         88.9          56.5
+//   B1 H1 4K x 4K, d = 64                              128.8         121.4         146.6
+//   B4 H8 256 x 256, d = 64                            16.5          17.7          22.4
+//   B1 H16 1K x 1K, d = 64                             100.9         101.2         140.7
+//
+// Grids of at most half a workgroup per compute unit (16-row tiles) take 8
+// rows per workgroup, each row split over 8 lanes, and sixteen key streams:
+// the shortest chain per wave, and the doubled grid still fits the GPU.
+// Long keys on grids of up to one workgroup per unit take sixteen streams of
+// 16 rows; everything else eight streams of 16 rows, whose workgroups are
+// the cheapest to start and merge.
 constexpr int kWideMinKeys = 512;
 
-template <int D, bool CAUSAL, int STREAMS>
-hipError_t launch_s(const Problem& p, int n_qtiles, hipStream_t stream) {
+template <int D, bool CAUSAL, int STREAMS, int QL>
+hipError_t launch_s(const Problem& p, hipStream_t stream) {
+    constexpr int ROWS = rows_of<QL>();
+    const int n_qtiles = (p.nq + ROWS - 1) / ROWS;
     const long long blocks = (long long)p.bh * n_qtiles;
-    return launch_kernel(prefill_f32_kernel<D, CAUSAL, STREAMS>, dim3((unsigned)blocks),
+    return launch_kernel(prefill_f32_kernel<D, CAUSAL, STREAMS, QL>, dim3((unsigned)blocks),
                          dim3(threads_of<STREAMS>()), stream, static_cast<const float*>(p.q),
                          static_cast<const float*>(p.k), static_cast<const float*>(p.v),
                          static_cast<float*>(p.o), p.lse, p.nq, p.nk, n_qtiles,
@@ -205,13 +222,13 @@ hipError_t launch_s(const Problem& p, int n_qtiles, hipStream_t stream) {
 
 template <int D, bool CAUSAL>
 hipError_t launch(const Problem& p, hipStream_t stream) {
-    const int n_qtiles = (p.nq + ROWS - 1) / ROWS;
+    const long long blocks16 = (long long)p.bh * ((p.nq + 15) / 16);
     int cus = 0;
     const hipError_t e = pf::device_cus(stream, cus);
     if (e != hipSuccess) return e;
-    if (p.nk >= kWideMinKeys && (long long)p.bh * n_qtiles <= cus)
-        return launch_s<D, CAUSAL, 16>(p, n_qtiles, stream);
-    return launch_s<D, CAUSAL, 8>(p, n_qtiles, stream);
+    if (2 * blocks16 <= cus) return launch_s<D, CAUSAL, 16, 8>(p, stream);
+    if (p.nk >= kWideMinKeys && blocks16 <= cus) return launch_s<D, CAUSAL, 16, 4>(p, stream);
+    return launch_s<D, CAUSAL, 8, 4>(p, stream);
 }
 
 template <int D>
@@ -221,7 +238,7 @@ hipError_t launch_d(const Problem& p, hipStream_t stream) {
 
 }  // namespace
 
-static_assert(ROWS == kPrefillF32RowsPerBlock, "row tile mismatch");
+static_assert(rows_of<4>() == kPrefillF32RowsPerBlock, "row tile mismatch");
 
 hipError_t launch_prefill_f32(const Problem& p, hipStream_t stream) {
     if (p.d == 64) return launch_d<64>(p, stream);

@@ -39,6 +39,7 @@ PREFILL_SHAPES = [
     (1, 2, 17, 64, 64),        # one full key tile: the single-tile ping-pong launch
     (1, 2, 64, 64, 128),
     (2, 9, 250, 600, 64),      # fp32: long keys on more workgroups than compute units
+    (1, 4, 1000, 1000, 64),    # fp32: long keys on at most one workgroup per compute unit
 ]
 
 
