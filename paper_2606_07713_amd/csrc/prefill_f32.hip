@@ -4,7 +4,7 @@
 // Used where the inputs are fp32 and the result must stay within fp32
 // rounding of the exact attention (no bf16 rounding of any operand).  One
 // workgroup owns a tile of query rows of one (batch*head); each row is
-// handled by QL lanes that split d (4 or 8).  The waves of a workgroup hold
+// handled by QL lanes that split d (4, 8 or 16).  The waves of a workgroup hold
 // the same rows and walk disjoint key streams (wave w takes tiles w,
 // w + STREAMS, ...; 128 keys per round of the workgroup), each staging its
 // own K/V tiles in its own LDS area, read by its lanes as broadcasts.  At the
@@ -189,23 +189,25 @@ __global__ __launch_bounds__(threads_of<STREAMS>()) void prefill_f32_kernel(
     }
 }
 
-// Three shapes of workgroup, by grid size (raw C-ABI calls, us, one box):
+// Four shapes of workgroup, by grid size (raw C-ABI calls, us, one box):
 //
-//   shape (streams x key tile, lanes per row, rows)   8x16, 4, 16   16x8, 4, 16   16x8, 8, 8
-//   B1 H1 128 x 128, d = 64                            6.39          6.83          4.97
-//   B1 H1 128 x 128, d = 128                           9.73          10.27         6.73
-//   B1 H2 300 x 517, d = 128                           31.7          27.9          17.2
-//   B1 H1 2K x 2K causal, d = 128                      103.1         88.9          56.5
-//   B1 H1 4K x 4K, d = 64                              128.8         121.4         146.6
-//   B4 H8 256 x 256, d = 64                            16.5          17.7          22.4
-//   B1 H16 1K x 1K, d = 64                             100.9         101.2         140.7
+//   streams x key tile, lanes per row, rows   8x16,4,16  16x8,4,16  16x8,8,8  16x8,16,4
+//   B1 H1 128 x 128, d = 64                    6.39       6.83       4.97      4.57
+//   B1 H1 128 x 128, d = 128                   9.73       10.27      6.73      5.40
+//   B1 H2 300 x 517, d = 128                   31.7       27.9       17.1      13.3
+//   B1 H1 1K x 1K causal, d = 64               -          -          17.2      14.5
+//   B1 H1 2K x 2K causal, d = 128              103.1      88.9       56.5      56.4
+//   B1 H1 4K x 4K, d = 64                      128.8      121.4      146.6     -
+//   B4 H8 256 x 256, d = 64                    16.5       17.7       22.4      -
+//   B1 H16 1K x 1K, d = 64                     100.9      101.2      140.7     -
 //
-// Grids of at most half a workgroup per compute unit (16-row tiles) take 8
-// rows per workgroup, each row split over 8 lanes, and sixteen key streams:
-// the shortest chain per wave, and the doubled grid still fits the GPU.
-// Long keys on grids of up to one workgroup per unit take sixteen streams of
-// 16 rows; everything else eight streams of 16 rows, whose workgroups are
-// the cheapest to start and merge.
+// Splitting a row over more lanes shortens each wave's chain and multiplies
+// the grid; it pays while the grid still fits the GPU.  So: 16 lanes per row
+// (4 rows per workgroup) while that grid fits the compute units, else 8 lanes
+// (8 rows) while that one does, all with sixteen key streams; long keys on
+// grids of up to one 16-row workgroup per unit take sixteen streams of 16
+// rows; everything else eight streams of 16 rows, whose workgroups are the
+// cheapest to start and merge.
 constexpr int kWideMinKeys = 512;
 
 template <int D, bool CAUSAL, int STREAMS, int QL>
@@ -226,6 +228,7 @@ hipError_t launch(const Problem& p, hipStream_t stream) {
     int cus = 0;
     const hipError_t e = pf::device_cus(stream, cus);
     if (e != hipSuccess) return e;
+    if (4 * blocks16 <= cus) return launch_s<D, CAUSAL, 16, 16>(p, stream);
     if (2 * blocks16 <= cus) return launch_s<D, CAUSAL, 16, 8>(p, stream);
     if (p.nk >= kWideMinKeys && blocks16 <= cus) return launch_s<D, CAUSAL, 16, 4>(p, stream);
     return launch_s<D, CAUSAL, 8, 4>(p, stream);

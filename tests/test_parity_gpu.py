@@ -40,6 +40,7 @@ PREFILL_SHAPES = [
     (1, 2, 64, 64, 128),
     (2, 9, 250, 600, 64),      # fp32: long keys on more workgroups than compute units
     (1, 4, 1000, 1000, 64),    # fp32: long keys on at most one workgroup per compute unit
+    (1, 6, 300, 300, 64),      # fp32: 8 lanes per row (grid of a quarter to a half of the GPU)
 ]
 
 
