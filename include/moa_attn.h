@@ -72,7 +72,10 @@ enum {
  * library's choice, which this function then reports for) and combine the
  * partial softmax results in a second pass need a workspace for those
  * partials: B*H*Nq*splits rows of dv + 2 fp32 values, rounded up to 256
- * bytes.  Decode-shaped calls (Nq == 1) always split.  bf16 prefill calls
+ * bytes.  Decode-shaped calls (Nq == 1) split when the library's choice (or
+ * `num_splits` > 1) says so: automatically so that B*H*splits reaches about
+ * 256 workgroups with at least 256 keys per split; with one split the call
+ * writes O directly and needs no workspace.  bf16 prefill calls
  * (Nq > 1) split when the library's choice (or `num_splits` > 1) says so:
  * automatically only for grids too small to fill the GPU (fewer than 128
  * tiles of 256 queries over all B*H slices, and at least 2048 keys), where
@@ -114,14 +117,15 @@ int moa_attn_num_splits(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t dk
  * workspace, workspace_bytes
  *           device scratch for calls that split their keys; at least
  *           moa_attn_workspace_bytes(...) bytes, 16-byte aligned, not
- *           overlapping any tensor.  Required for decode-shaped calls and
- *           for bf16 prefill with num_splits > 1 (else MOA_ERR_WORKSPACE);
+ *           overlapping any tensor.  Required for decode-shaped calls that
+ *           split and for bf16 prefill with num_splits > 1 (else
+ *           MOA_ERR_WORKSPACE);
  *           a bf16 prefill call with num_splits == 0 whose workspace is
  *           missing or too small runs in one pass instead.  May be NULL/0
  *           when moa_attn_workspace_bytes(...) is 0.
  * num_splits
  *           key splits across workgroups (0 = library's choice, else
- *           1..256; 1 = no split for prefill).  Ignored by fp32 prefill.
+ *           1..256; 1 = no split).  Ignored by fp32 prefill.
  * stream    hipStream_t as void*.
  *
  * Computation: inner products and softmax statistics in fp32 from exact

@@ -83,7 +83,9 @@ size_t prefill_ws_bytes(int64_t bh, int64_t Nq, int64_t d, int splits) {
 // Name of the HIP error behind the last MOA_ERR_HIP returned on this thread.
 thread_local const char* g_last_hip_error = "hipSuccess";
 
+// A decode call with one split writes O directly and needs no workspace.
 size_t decode_ws_bytes(int64_t bh, int64_t d, int splits) {
+    if (splits <= 1) return 0;
     return align256((size_t)bh * (size_t)splits * (size_t)(d + 2) * sizeof(float));
 }
 
@@ -263,7 +265,7 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, i
     if (decode && bh > 0) {
         splits = pick_splits(bh, Nk, num_splits);
         need = decode_ws_bytes(bh, dk, splits);
-        if (!ws_fits(need)) return short_ws;
+        if (need && !ws_fits(need)) return short_ws;
     } else if (!decode && bh > 0 && Nq > 0 && in_dtype == MOA_BF16) {
         // Split-K prefill: explicitly requested splits need the workspace;
         // the automatic choice falls back to one pass without it.

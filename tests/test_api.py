@@ -73,11 +73,12 @@ def test_workspace_and_splits():
     assert moa.moa_attn_num_splits(1, 32, 128, 32768, 128, 128, 1) == 1
     assert moa.moa_attn_workspace_bytes(1, 32, 128, 32768, 128, 128, 1) == 0
     assert moa.moa_attn_workspace_bytes(1, 1, 100, 300, 64, 64, 3) == -(-100 * 3 * 66 * 4 // 256) * 256
-    # decode: partials of bh*splits rows of (d + 2) floats, rounded up to 256 B
-    s = moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 0)
-    assert 1 <= s <= 256
-    ws = moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 0)
-    assert ws >= 64 * 32 * s * 130 * 4 and ws % 256 == 0
+    # decode: partials of bh*splits rows of (d + 2) floats, rounded up to 256 B;
+    # one split writes O directly and needs none
+    assert moa.moa_attn_num_splits(4, 32, 1, 32768, 128, 128, 0) == 2
+    assert moa.moa_attn_workspace_bytes(4, 32, 1, 32768, 128, 128, 0) == -(-4 * 32 * 2 * 130 * 4 // 256) * 256
+    assert moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 0) == 0
+    assert moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 1) == 0
     assert moa.moa_attn_num_splits(64, 32, 1, 8192, 128, 128, 5) == 5
     assert moa.moa_attn_workspace_bytes(64, 32, 1, 8192, 128, 128, 5) >= 64 * 32 * 5 * 130 * 4
     # short key ranges are not split below the minimum chunk
@@ -115,9 +116,9 @@ def _call(**kw):
     (dict(O=A + 64), 1),                               # O overlaps Q
     (dict(num_splits=-1), 1), (dict(num_splits=257), 1),
     (dict(dk=96, dv=96), 2), (dict(dk=64, dv=128), 2), (dict(dk=256, dv=256), 2),
-    (dict(Nq=1), 3),                                   # decode needs a workspace
-    (dict(Nq=1, workspace=W, workspace_bytes=16), 3),
-    (dict(Nq=1, workspace=A, workspace_bytes=1 << 20), 1),   # workspace overlaps Q
+    (dict(Nq=1, num_splits=2), 3),                     # a split decode needs a workspace
+    (dict(Nq=1, num_splits=2, workspace=W, workspace_bytes=16), 3),
+    (dict(Nq=1, num_splits=2, workspace=A, workspace_bytes=1 << 20), 1),   # workspace overlaps Q
     (dict(num_splits=2), 3),                           # explicit prefill splits need a workspace
     (dict(num_splits=2, workspace=W, workspace_bytes=256), 3),
     (dict(num_splits=2, workspace=D, workspace_bytes=1 << 20), 1),   # workspace overlaps O
@@ -304,10 +305,10 @@ def test_noalloc_validation():
     assert _call_noalloc(Q=(1 << 40) + 8) == moa.MOA_ERR_INVALID_ARG
     assert _call_noalloc(dk=96, dv=96) == moa.MOA_ERR_UNSUPPORTED
     assert _call_noalloc(causal=1, Nq=9000, Nk=8192) == moa.MOA_ERR_INVALID_ARG
-    # decode whose partial states exceed the fixed array: 65536 heads x 1 split x 130 floats
-    need = moa.moa_attn_workspace_bytes(256, 256, 1, 256, 128, 128, 0)
+    # decode whose partial states exceed the fixed array: 65536 heads x 2 splits x 130 floats
+    need = moa.moa_attn_workspace_bytes(256, 256, 1, 512, 128, 128, 2)
     assert need > moa.MOA_NOALLOC_SCRATCH_BYTES
-    assert _call_noalloc(B=256, H=256, Nk=256) == moa.MOA_ERR_SCRATCH
+    assert _call_noalloc(B=256, H=256, Nk=512, num_splits=2) == moa.MOA_ERR_SCRATCH
     # explicit prefill splits beyond the array are rejected too
     need = moa.moa_attn_workspace_bytes(1, 32, 2048, 65536, 128, 128, 8)
     assert need > moa.MOA_NOALLOC_SCRATCH_BYTES
