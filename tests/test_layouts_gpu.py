@@ -108,7 +108,10 @@ SHAPES = {
     "pingpong": (2, 128, 1000, 1000, 64, "bf16"),    # 1024 items of 256 queries
     "pingpong_mid": (1, 128, 600, 600, 128, "bf16"), # 384 items: 1.5 per compute unit
     "keysplit": (2, 4, 300, 300, 128, "bf16"),       # 16 items
-    "f32": (2, 3, 100, 100, 64, "f32"),
+    "f32": (2, 3, 100, 100, 64, "f32"),              # fp32 workgroup shapes by grid size:
+    "f32_mid": (1, 6, 300, 300, 64, "f32"),          #   16 lanes per row above, 8 here,
+    "f32_wide": (1, 4, 1000, 1000, 128, "f32"),      #   4 lanes in 16 key streams,
+    "f32_large": (2, 9, 250, 600, 64, "f32"),        #   4 lanes in 8 key streams
     "decode": (4, 8, 1, 3000, 128, "bf16"),
 }
 
